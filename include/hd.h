@@ -1,0 +1,130 @@
+/*
+ * hd.h — C ABI of the MI355X (gfx950) batched hyperdimensional-computing
+ * inference library.
+ *
+ * The operation is the two-stage HDC inference of ScalableHD (Sec. II-D,
+ * Alg. 1): with raw features X[N,F], base hypervectors B[F,D] and class
+ * hypervectors C[K,D] (the paper's M),
+ *   Stage I  (Eq. 7, Eq. 2-3):  H = HardSign(X B),  HardSign(x) = +1 if x >= 0 else -1 (Eq. 1)
+ *   Stage II (Eq. 8, Eq. 9):    S = H C^T,  labels[n] = argmax_k S[n,k]
+ *
+ * Conventions shared by every entry point:
+ *   - Layout: dense, contiguous, row-major. X[N,F], B[F,D], C[K,D], H[N,D],
+ *     scores[N,K]. The paper's J = M^T is C read column-major.
+ *   - Types: hd_dtype names the element type of X, B and C (HD_BF16 buffers
+ *     hold raw bfloat16 bit patterns). Accumulation is always fp32. H and
+ *     scores are fp32; labels are int32 in [0, K).
+ *   - Pointers: X, B, C, H, labels, scores, workspace and packed models are
+ *     DEVICE pointers owned by the caller. The library allocates nothing,
+ *     frees nothing and keeps no pointer after a call returns. Outputs must
+ *     not alias inputs.
+ *   - Streams: work is enqueued on `stream` (0 = the null stream) and the call
+ *     returns without synchronising; results are valid once the stream has
+ *     reached that point.
+ *   - Errors: arguments are validated on the host before anything is
+ *     enqueued; a failing call enqueues nothing. N == 0 is a no-op returning
+ *     HD_OK. HD_ERR_HIP reports a launch failure (hipGetLastError).
+ *   - Ties: HardSign(0) = +1 (Eq. 1: ties broken toward +1, so -0.0 -> +1);
+ *     argmax ties go to the lowest class index (the paper is silent; this is
+ *     the first-maximum convention).
+ *   - Limits: 1 <= F, D, K <= 2^30 and 0 <= N <= 2^30; anything larger
+ *     returns HD_ERR_UNSUPPORTED.
+ *   - Thread safety: the library holds no mutable global state; concurrent
+ *     calls are safe when each uses its own workspace.
+ */
+#ifndef HD_H_
+#define HD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *hipStream_t;
+
+typedef enum {
+  HD_OK = 0,
+  HD_ERR_ARG = 1,         /* null pointer, negative/zero size, bad enum */
+  HD_ERR_UNSUPPORTED = 2, /* size or dtype/act combination beyond what is built */
+  HD_ERR_WORKSPACE = 3,   /* workspace or packed buffer too small */
+  HD_ERR_HIP = 4          /* a HIP launch failed */
+} hd_status;
+
+typedef enum { HD_F32 = 0, HD_BF16 = 1 } hd_dtype;
+
+/* HD_ACT_HARDSIGN is the paper's encoding activation (Sec. II-B, Eq. 3).
+ * HD_ACT_IDENTITY skips it (H = X B): a linear test mode, S = X B C^T. */
+typedef enum { HD_ACT_HARDSIGN = 0, HD_ACT_IDENTITY = 1 } hd_act;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *hd_status_str(hd_status s);
+
+/*
+ * Stage I alone (Alg. 1 Stage I; Eq. 7 with the activation of Eq. 1):
+ *   H[n,d] = act( sum_f X[n,f] * B[f,d] )      written as fp32 to H[N,D].
+ * This entry point materialises H in device memory; it exists for tests and
+ * for composing the stages by hand. hd_infer never materialises H.
+ */
+hd_status hd_encode(const void *X, const void *B, float *H, int64_t N, int64_t F, int64_t D,
+                    hd_dtype dt, hd_act act, hipStream_t stream);
+
+/*
+ * Stage II alone (Alg. 1 Stage II; Eq. 8 and Eq. 9) on a real matrix H[N,D]:
+ *   S[n,k] = sum_d H[n,d] * C[k,d];  labels[n] = lowest k maximising S[n,k].
+ * C has element type c_dt. scores may be NULL (then only labels are written).
+ */
+hd_status hd_similarity(const float *H, const void *C, int32_t *labels, float *scores, int64_t N,
+                        int64_t D, int64_t K, hd_dtype c_dt, hipStream_t stream);
+
+/* Bytes of device workspace hd_infer needs for these sizes (0 is possible). */
+size_t hd_infer_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt);
+
+/*
+ * Alg. 1 end to end, fused: labels[N] (and scores[N,K] when non-NULL) from
+ * X, B, C, with the encoded matrix H never written to device memory.
+ * workspace: caller-owned device buffer of at least
+ *   hd_infer_workspace_bytes(N, F, D, K, dt) bytes, ZEROED BY THE CALLER
+ *   BEFORE ITS FIRST USE. Every call leaves the parts that must start at zero
+ *   zeroed again, so a workspace can be reused by consecutive calls on one
+ *   stream without clearing. Calls that overlap in time must not share a
+ *   workspace. May be NULL only when the required size is 0.
+ * The small-batch path splits the hypervector dimension D across workgroups
+ * (the paper's small-batch variant, Sec. III-C Alg. 3) and reduces partial
+ * scores with fp32 atomics, so score low bits can vary from run to run; the
+ * large-batch path splits the batch (the large-batch variant, Alg. 4) and
+ * repacks B and C into the workspace first (the parameter tiling of
+ * Sec. III-D) unless a packed model is supplied through hd_infer_packed.
+ */
+hd_status hd_infer(const void *X, const void *B, const void *C, int32_t *labels, float *scores,
+                   int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,
+                   void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * One-time model tiling (Sec. III-D: B and J = M^T stored in the block order
+ * the consumer reads them). The packed image is opaque; its size depends only
+ * on (F, D, K, dt). packed must be a device buffer of at least
+ * hd_model_packed_bytes(F, D, K, dt) bytes.
+ */
+size_t hd_model_packed_bytes(int64_t F, int64_t D, int64_t K, hd_dtype dt);
+hd_status hd_pack_model(const void *B, const void *C, int64_t F, int64_t D, int64_t K, hd_dtype dt,
+                        void *packed, size_t packed_bytes, hipStream_t stream);
+
+/* Bytes of workspace hd_infer_packed needs (no room for a packed model). */
+size_t hd_infer_packed_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt);
+
+/*
+ * Alg. 1 end to end from a model packed by hd_pack_model with the same
+ * (F, D, K, dt). X is read as given (row-major, never pre-packed). Same
+ * workspace and output rules as hd_infer.
+ */
+hd_status hd_infer_packed(const void *X, const void *packed, int32_t *labels, float *scores,
+                          int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,
+                          void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HD_H_ */

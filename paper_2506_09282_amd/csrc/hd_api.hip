@@ -1,0 +1,165 @@
+// C ABI entry points: argument validation on the host (before anything is
+// enqueued), path selection, and kernel launch on the caller's stream.
+#include "../../include/hd.h"
+#include "hd_internal.hpp"
+
+namespace {
+
+constexpr int64_t kMaxDim = int64_t(1) << 30;
+
+bool dims_ok(int64_t N, int64_t F, int64_t D, int64_t K) {
+  return N <= kMaxDim && F <= kMaxDim && D <= kMaxDim && K <= kMaxDim;
+}
+
+bool enums_ok(int dt, int act) { return (dt == HD_F32 || dt == HD_BF16) && (act == 0 || act == 1); }
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+bool use_small(int64_t N) { return N <= hd::kSmallMaxN; }
+
+hd_status from_hip(hipError_t e) { return e == hipSuccess ? HD_OK : HD_ERR_HIP; }
+
+size_t esize(int dt) { return dt == HD_F32 ? 4 : 2; }
+
+// Packed model image: [tiled B and C for the matrix-core path | B as given |
+// C as given]. The natural-layout copies serve the small-batch path, which
+// streams B row segments directly.
+struct Image {
+  size_t tiled, raw_b, raw_c, total;
+};
+
+Image image_layout(int64_t F, int64_t D, int64_t K, int dt) {
+  Image im;
+  im.tiled = align256(hd::large_packed_bytes(F, D, K, dt));
+  im.raw_b = align256((size_t)F * D * esize(dt));
+  im.raw_c = align256((size_t)K * D * esize(dt));
+  im.total = im.tiled + im.raw_b + im.raw_c;
+  return im;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hd_status_str(hd_status s) {
+  switch (s) {
+    case HD_OK:
+      return "HD_OK";
+    case HD_ERR_ARG:
+      return "HD_ERR_ARG: invalid argument";
+    case HD_ERR_UNSUPPORTED:
+      return "HD_ERR_UNSUPPORTED: size or type combination not supported";
+    case HD_ERR_WORKSPACE:
+      return "HD_ERR_WORKSPACE: workspace or packed buffer too small";
+    case HD_ERR_HIP:
+      return "HD_ERR_HIP: HIP launch failed";
+  }
+  return "HD_ERR_UNKNOWN";
+}
+
+hd_status hd_encode(const void* X, const void* B, float* H, int64_t N, int64_t F, int64_t D,
+                    hd_dtype dt, hd_act act, hipStream_t stream) {
+  if (N < 0 || F < 1 || D < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
+  if (!dims_ok(N, F, D, 1)) return HD_ERR_UNSUPPORTED;
+  if (N == 0) return HD_OK;
+  if (!X || !B || !H) return HD_ERR_ARG;
+  return from_hip(hd::launch_encode(X, B, H, N, F, D, dt, act, stream));
+}
+
+hd_status hd_similarity(const float* H, const void* C, int32_t* labels, float* scores, int64_t N,
+                        int64_t D, int64_t K, hd_dtype c_dt, hipStream_t stream) {
+  if (N < 0 || D < 1 || K < 1 || !enums_ok(c_dt, 0)) return HD_ERR_ARG;
+  if (!dims_ok(N, 1, D, K)) return HD_ERR_UNSUPPORTED;
+  if (N == 0) return HD_OK;
+  if (!H || !C || !labels) return HD_ERR_ARG;
+  return from_hip(hd::launch_similarity(H, C, labels, scores, N, D, K, c_dt, stream));
+}
+
+size_t hd_model_packed_bytes(int64_t F, int64_t D, int64_t K, hd_dtype dt) {
+  if (F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(0, F, D, K)) return 0;
+  return image_layout(F, D, K, dt).total;
+}
+
+size_t hd_infer_packed_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
+  if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
+  if (use_small(N)) return hd::small_workspace_bytes(N, F, D, K);
+  return hd::large_workspace_bytes(N, F, D, K, dt);
+}
+
+size_t hd_infer_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
+  if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
+  if (use_small(N)) return hd::small_workspace_bytes(N, F, D, K);
+  return align256(hd::large_packed_bytes(F, D, K, dt)) +
+         hd::large_workspace_bytes(N, F, D, K, dt);
+}
+
+hd_status hd_pack_model(const void* B, const void* C, int64_t F, int64_t D, int64_t K, hd_dtype dt,
+                        void* packed, size_t packed_bytes, hipStream_t stream) {
+  if (F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0)) return HD_ERR_ARG;
+  if (!dims_ok(0, F, D, K)) return HD_ERR_UNSUPPORTED;
+  if (!B || !C || !packed) return HD_ERR_ARG;
+  const Image im = image_layout(F, D, K, dt);
+  if (packed_bytes < im.total) return HD_ERR_WORKSPACE;
+  char* p = static_cast<char*>(packed);
+  if (hd::launch_pack(B, C, F, D, K, dt, p, stream) != hipSuccess) return HD_ERR_HIP;
+  if (hipMemcpyAsync(p + im.tiled, B, (size_t)F * D * esize(dt), hipMemcpyDeviceToDevice,
+                     stream) != hipSuccess)
+    return HD_ERR_HIP;
+  if (hipMemcpyAsync(p + im.tiled + im.raw_b, C, (size_t)K * D * esize(dt),
+                     hipMemcpyDeviceToDevice, stream) != hipSuccess)
+    return HD_ERR_HIP;
+  return HD_OK;
+}
+
+static hd_status infer_common(const void* X, const void* B, const void* C, const void* packed,
+                              int32_t* labels, float* scores, int64_t N, int64_t F, int64_t D,
+                              int64_t K, hd_dtype dt, hd_act act, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+  if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
+  if (!dims_ok(N, F, D, K)) return HD_ERR_UNSUPPORTED;
+  if (N == 0) return HD_OK;
+  if (!X || !labels || (packed ? false : (!B || !C))) return HD_ERR_ARG;
+  const bool small = use_small(N);
+  if (!small && !hd::large_supported(N, F, D, K, dt)) return HD_ERR_UNSUPPORTED;
+  const size_t need = packed ? hd_infer_packed_workspace_bytes(N, F, D, K, dt)
+                             : hd_infer_workspace_bytes(N, F, D, K, dt);
+  if (need > 0 && !workspace) return HD_ERR_ARG;
+  if (workspace_bytes < need) return HD_ERR_WORKSPACE;
+
+  if (small) {
+    if (packed) {
+      const Image im = image_layout(F, D, K, dt);
+      B = static_cast<const char*>(packed) + im.tiled;
+      C = static_cast<const char*>(packed) + im.tiled + im.raw_b;
+    }
+    return from_hip(
+        hd::launch_small(X, B, C, labels, scores, N, F, D, K, dt, act, workspace, stream));
+  }
+  void* large_ws = workspace;
+  if (!packed) {
+    const size_t pb = align256(hd::large_packed_bytes(F, D, K, dt));
+    const hipError_t e = hd::launch_pack(B, C, F, D, K, dt, workspace, stream);
+    if (e != hipSuccess) return HD_ERR_HIP;
+    packed = workspace;
+    large_ws = static_cast<char*>(workspace) + pb;
+  }
+  return from_hip(
+      hd::launch_large(X, packed, labels, scores, N, F, D, K, dt, act, large_ws, stream));
+}
+
+hd_status hd_infer(const void* X, const void* B, const void* C, int32_t* labels, float* scores,
+                   int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return infer_common(X, B, C, nullptr, labels, scores, N, F, D, K, dt, act, workspace,
+                      workspace_bytes, stream);
+}
+
+hd_status hd_infer_packed(const void* X, const void* packed, int32_t* labels, float* scores,
+                          int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (N > 0 && !packed) return HD_ERR_ARG;
+  return infer_common(X, nullptr, nullptr, packed, labels, scores, N, F, D, K, dt, act, workspace,
+                      workspace_bytes, stream);
+}
+
+}  // extern "C"

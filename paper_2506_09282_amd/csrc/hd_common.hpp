@@ -1,0 +1,61 @@
+// Internal device helpers shared by the HDC inference kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hd {
+
+typedef uint16_t bf16raw;  // raw bfloat16 bit pattern
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// Element loads widened to fp32 (exact for both storage types).
+__device__ __forceinline__ float load_elem(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_elem(const bf16raw* p, int64_t i) {
+  return bf16_to_f32(p[i]);
+}
+
+// Four consecutive elements starting at p[i]; i must be a multiple of 4 and
+// the base 16-byte (fp32) / 8-byte (bf16) aligned.
+__device__ __forceinline__ float4 load4(const float* p, int64_t i) {
+  return *reinterpret_cast<const float4*>(p + i);
+}
+__device__ __forceinline__ float4 load4(const bf16raw* p, int64_t i) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p + i);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+
+// Eq. 1 of the paper: +1 for v >= 0 (so -0.0 gives +1), -1 otherwise
+// (NaN compares false and gives -1). A literal comparison, not a sign-bit test.
+__device__ __forceinline__ float hardsign(float v) { return v >= 0.0f ? 1.0f : -1.0f; }
+
+__device__ __forceinline__ float activate(float v, int act) { return act ? v : hardsign(v); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+// Loads that must observe other workgroups' device-scope atomics/stores
+// made before a release/acquire handshake.
+__device__ __forceinline__ float load_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__host__ __device__ constexpr int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace hd

@@ -1,0 +1,36 @@
+// Host-side declarations shared between the C-ABI layer and the launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hd {
+
+// Small-batch fused path (split-D across workgroups).
+constexpr int kSmallMaxN = 64;
+constexpr int kSmallCols = 32;   // hypervector columns per workgroup
+constexpr int kSmallReplicas = 32;
+
+size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K);
+hipError_t launch_small(const void* X, const void* B, const void* C, int32_t* labels,
+                        float* scores, int64_t N, int64_t F, int64_t D, int64_t K, int dt,
+                        int act, void* workspace, hipStream_t stream);
+
+// Unfused stages.
+hipError_t launch_encode(const void* X, const void* B, float* H, int64_t N, int64_t F, int64_t D,
+                         int dt, int act, hipStream_t stream);
+hipError_t launch_similarity(const float* H, const void* C, int32_t* labels, float* scores,
+                             int64_t N, int64_t D, int64_t K, int c_dt, hipStream_t stream);
+
+// Large-batch fused path (MFMA, packed model).
+bool large_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
+size_t large_packed_bytes(int64_t F, int64_t D, int64_t K, int dt);
+size_t large_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
+hipError_t launch_pack(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,
+                       void* packed, hipStream_t stream);
+hipError_t launch_large(const void* X, const void* packed, int32_t* labels, float* scores,
+                        int64_t N, int64_t F, int64_t D, int64_t K, int dt, int act,
+                        void* workspace, hipStream_t stream);
+
+}  // namespace hd

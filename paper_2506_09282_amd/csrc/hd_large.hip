@@ -1,0 +1,713 @@
+// Large-batch fused inference on the matrix cores: the GPU form of the
+// paper's large-batch variant (Sec. III-C, Alg. 4), which splits the batch N
+// across workers, each accumulating its rows of S over every column block of
+// the encoded matrix.
+//
+// Formulation. Stage I is computed transposed, V^T[d,n] = sum_f B^T[d,f] X[n,f],
+// so that the hypervector dimension d is the MFMA row index and the sample n
+// the column index. With the 32x32 MFMA accumulator layout each lane then
+// holds 16 d-values of one sample, which after HardSign (Eq. 1) are exactly a
+// B-operand fragment of the Stage II MFMA S^T[k,n] += C[k,d] H^T[d,n] (Eq. 8)
+// up to a fixed permutation of d. The permutation is absorbed into the tiled
+// copy of C, so the encoded block goes from accumulators to the next MFMA
+// without touching LDS or device memory: H is never materialised.
+//
+// Data layout. A workgroup owns NT = 32*NTILES samples; their rows of X are
+// copied once into LDS (zero padded) and stay resident while the workgroup
+// sweeps its slice of D. B and C are read from a tiled copy made once per
+// model (the parameter tiling of Sec. III-D): every MFMA A-fragment is one
+// contiguous, fully coalesced 1 KiB block, so B streams straight from L2 into
+// registers with a software-pipelined prefetch ring.
+//
+// Work split. Each of the 4 waves owns "units" of 64 hypervector dimensions
+// (two 32-row MFMA tiles) round-robin within the workgroup's D slice and keeps
+// its own partial S; the waves' partials are summed through LDS at the end.
+// When there are too few sample tiles to fill the GPU, D is also split into
+// DS slices whose partial scores are combined by the last-arriving workgroup
+// of each sample tile (ticket counter, self-cleaning).
+#include "hd_common.hpp"
+#include "hd_internal.hpp"
+
+namespace hd {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = 4;
+constexpr int kPrefetch = 4;  // f-steps of B fragments in flight per wave
+constexpr int kLdsBytes = 160 * 1024 - 256;  // leave room for static LDS
+
+template <typename U, typename V>
+__device__ __forceinline__ U bitcast(const V& v) {
+  static_assert(sizeof(U) == sizeof(V), "size");
+  U u;
+  __builtin_memcpy(&u, &v, sizeof(U));
+  return u;
+}
+
+// ---------------------------------------------------------------------------
+// Element-type traits. One "f-step" consumes one 16-byte fragment per lane of
+// both operands: 16 features for bf16 (one 32x32x16 MFMA), 8 features for
+// fp32 (four 32x32x2 MFMAs).
+// ---------------------------------------------------------------------------
+struct TrBF16 {
+  typedef bf16raw elem;
+  static constexpr int kFStep = 16;
+  static constexpr int kVec = 8;  // elements per 16-byte group
+  static constexpr int kEsz = 2;
+  static constexpr int kCFrags = 2;  // 1 KiB C fragments per (d-block, class block)
+  // LDS position of feature column c inside a sample row.
+  __device__ static int lds_pos(int c) { return c; }
+  __device__ static void stage1(f32x16& acc, const uint4& a, const uint4& b) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast<bf16x8>(a), bitcast<bf16x8>(b), acc,
+                                                  0, 0, 0);
+  }
+};
+
+struct TrF32 {
+  typedef float elem;
+  static constexpr int kFStep = 8;
+  static constexpr int kVec = 4;
+  static constexpr int kEsz = 4;
+  static constexpr int kCFrags = 4;
+  // Within each group of 8 features the even ones are stored first, so a
+  // lane of MFMA k-half g reads its four features (g, g+2, g+4, g+6) as one
+  // 16-byte word.
+  __device__ static int lds_pos(int c) {
+    const int r = c & 7;
+    return (c & ~7) + 4 * (r & 1) + (r >> 1);
+  }
+  __device__ static void stage1(f32x16& acc, const uint4& a, const uint4& b) {
+    const float4 af = bitcast<float4>(a), bf = bitcast<float4>(b);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.x, bf.x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.y, bf.y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.z, bf.z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.w, bf.w, acc, 0, 0, 0);
+  }
+};
+
+// Number of f-steps and padded row pitch (elements) of the LDS X tile.
+template <class Tr>
+__host__ __device__ inline int nfs_of(int F) {
+  return (F + Tr::kFStep - 1) / Tr::kFStep;
+}
+template <class Tr>
+__host__ __device__ inline int pitch_of(int F) {
+  // Padding by half a 16-byte group (bf16) / one group (fp32) keeps the
+  // 32 rows read by one fragment load on distinct LDS banks.
+  return nfs_of<Tr>(F) * Tr::kFStep + (Tr::kEsz == 2 ? 8 : 4);
+}
+
+// ---------------------------------------------------------------------------
+// Tiled model image.
+//   B tile (db, fs): 64 lanes x 16 bytes; lane l holds
+//     bf16: B[16fs + 8(l/32) + e][32db + l%32], e = 0..7
+//     fp32: B[8fs + 2j + l/32][32db + l%32],   j = 0..3
+//   C tile, bf16 (db, h, kb): lane l holds C[32kb + l%32][32db + 16h + 4(l/32) + e]
+//     for e = 0..3 and C[..][32db + 16h + 8 + 4(l/32) + e - 4] for e = 4..7
+//   C tile, fp32 (db, kb, q): lane l holds C[32kb + l%32][32db + 8q + 4(l/32) + j]
+// Out-of-range entries are zero. NDB is rounded up to even (64-dim units).
+// ---------------------------------------------------------------------------
+struct PackGeom {
+  int ndb, nfs, kb;
+  size_t b_bytes, c_bytes;
+};
+
+// Class blocks of 32 handled per launch: 1, 2 or 4.
+inline int kb_of(int64_t K) {
+  const int kb = (int)cdiv(K, 32);
+  return kb == 3 ? 4 : kb;
+}
+
+template <class Tr>
+PackGeom pack_geom(int64_t F, int64_t D, int64_t K) {
+  PackGeom g;
+  g.ndb = (int)(cdiv(D, 64) * 2);
+  g.nfs = nfs_of<Tr>((int)F);
+  g.kb = kb_of(K);
+  g.b_bytes = (size_t)g.ndb * g.nfs * 1024;
+  g.c_bytes = (size_t)g.ndb * g.kb * Tr::kCFrags * 1024;
+  return g;
+}
+
+__global__ void pack_b_bf16(const bf16raw* __restrict__ B, uint4* __restrict__ Bp, int F, int D,
+                            int ndb, int nfs) {
+  const int64_t frag = blockIdx.x;
+  const int l = threadIdx.x;
+  if (frag >= (int64_t)ndb * nfs) return;
+  const int db = (int)(frag / nfs), fs = (int)(frag % nfs);
+  const int d = 32 * db + (l & 31);
+  uint16_t v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int f = 16 * fs + 8 * (l >> 5) + e;
+    v[e] = (f < F && d < D) ? B[(int64_t)f * D + d] : (uint16_t)0;
+  }
+  Bp[frag * 64 + l] = make_uint4(v[0] | (uint32_t)v[1] << 16, v[2] | (uint32_t)v[3] << 16,
+                                 v[4] | (uint32_t)v[5] << 16, v[6] | (uint32_t)v[7] << 16);
+}
+
+__global__ void pack_b_f32(const float* __restrict__ B, uint4* __restrict__ Bp, int F, int D,
+                           int ndb, int nfs) {
+  const int64_t frag = blockIdx.x;
+  const int l = threadIdx.x;
+  if (frag >= (int64_t)ndb * nfs) return;
+  const int db = (int)(frag / nfs), fs = (int)(frag % nfs);
+  const int d = 32 * db + (l & 31);
+  float v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int f = 8 * fs + 2 * j + (l >> 5);
+    v[j] = (f < F && d < D) ? B[(int64_t)f * D + d] : 0.0f;
+  }
+  Bp[frag * 64 + l] = make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
+                                 __float_as_uint(v[2]), __float_as_uint(v[3]));
+}
+
+// grid: ndb * 2 * kb fragments of 64 lanes.
+__global__ void pack_c_bf16(const bf16raw* __restrict__ C, uint4* __restrict__ Cp, int D, int K,
+                            int ndb, int kb) {
+  const int64_t frag = blockIdx.x;
+  const int l = threadIdx.x;
+  if (frag >= (int64_t)ndb * 2 * kb) return;
+  const int kbi = (int)(frag % kb);
+  const int h = (int)((frag / kb) % 2);
+  const int db = (int)(frag / (2 * kb));
+  const int k = 32 * kbi + (l & 31);
+  uint16_t v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int d = 32 * db + 16 * h + 4 * (l >> 5) + (e < 4 ? e : 8 + e - 4);
+    v[e] = (k < K && d < D) ? C[(int64_t)k * D + d] : (uint16_t)0;
+  }
+  Cp[frag * 64 + l] = make_uint4(v[0] | (uint32_t)v[1] << 16, v[2] | (uint32_t)v[3] << 16,
+                                 v[4] | (uint32_t)v[5] << 16, v[6] | (uint32_t)v[7] << 16);
+}
+
+// grid: ndb * kb * 4 fragments of 64 lanes.
+__global__ void pack_c_f32(const float* __restrict__ C, uint4* __restrict__ Cp, int D, int K,
+                           int ndb, int kb) {
+  const int64_t frag = blockIdx.x;
+  const int l = threadIdx.x;
+  if (frag >= (int64_t)ndb * kb * 4) return;
+  const int q = (int)(frag % 4);
+  const int kbi = (int)((frag / 4) % kb);
+  const int db = (int)(frag / (4 * kb));
+  const int k = 32 * kbi + (l & 31);
+  float v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int d = 32 * db + 8 * q + 4 * (l >> 5) + j;
+    v[j] = (k < K && d < D) ? C[(int64_t)k * D + d] : 0.0f;
+  }
+  Cp[frag * 64 + l] = make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
+                                 __float_as_uint(v[2]), __float_as_uint(v[3]));
+}
+
+// ---------------------------------------------------------------------------
+// Stage II on one finished 32x32 V^T tile (rows d of block db, columns n of
+// one sample tile): activation, then accumulate S^T for every class block.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+  // round-to-nearest-even fp32 -> bf16 for finite values
+  uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
+  ua = (ua + 0x7fffu + ((ua >> 16) & 1u)) >> 16;
+  ub = (ub + 0x7fffu + ((ub >> 16) & 1u)) >> 16;
+  return ua | (ub << 16);
+}
+
+__device__ __forceinline__ uint32_t sign_pair(float a, float b) {
+  const uint32_t lo = a >= 0.0f ? 0x3F80u : 0xBF80u;
+  const uint32_t hi = b >= 0.0f ? 0x3F80u : 0xBF80u;
+  return lo | (hi << 16);
+}
+
+template <int KB>
+__device__ __forceinline__ void stage2_bf16(const f32x16& v, const uint4 (&cfr)[2][KB],
+                                            f32x16 (&s)[KB], int act) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (!act) {
+      uint4 hb;
+      hb.x = sign_pair(v[8 * h + 0], v[8 * h + 1]);
+      hb.y = sign_pair(v[8 * h + 2], v[8 * h + 3]);
+      hb.z = sign_pair(v[8 * h + 4], v[8 * h + 5]);
+      hb.w = sign_pair(v[8 * h + 6], v[8 * h + 7]);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast<bf16x8>(cfr[h][kb]),
+                                                        bitcast<bf16x8>(hb), s[kb], 0, 0, 0);
+    } else {
+      // Identity test mode: split v into three bf16 terms (about 24 bits).
+      float r[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) r[e] = v[8 * h + e];
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+        uint4 hb;
+        hb.x = pack2_bf16(r[0], r[1]);
+        hb.y = pack2_bf16(r[2], r[3]);
+        hb.z = pack2_bf16(r[4], r[5]);
+        hb.w = pack2_bf16(r[6], r[7]);
+        const uint32_t w[4] = {hb.x, hb.y, hb.z, hb.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t bits = (w[e >> 1] >> (16 * (e & 1))) & 0xffffu;
+          r[e] -= __uint_as_float(bits << 16);
+        }
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast<bf16x8>(cfr[h][kb]),
+                                                          bitcast<bf16x8>(hb), s[kb], 0, 0, 0);
+      }
+    }
+  }
+}
+
+template <int KB>
+__device__ __forceinline__ void stage2_f32(const f32x16& v, const uint4 (&cfr)[KB][4],
+                                           f32x16 (&s)[KB], int act) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float h = act ? v[4 * q + j] : hardsign(v[4 * q + j]);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const float c = __uint_as_float(j == 0 ? cfr[kb][q].x
+                                         : j == 1 ? cfr[kb][q].y
+                                         : j == 2 ? cfr[kb][q].z
+                                                  : cfr[kb][q].w);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(c, h, s[kb], 0, 0, 0);
+      }
+    }
+  }
+}
+
+// C fragments of one 64-dim unit (two d-blocks).
+template <class Tr, int KB>
+struct CFrags;
+template <int KB>
+struct CFrags<TrBF16, KB> {
+  uint4 f[2][2][KB];  // [db2][h][kb]
+  __device__ void load(const uint4* __restrict__ Cp, int db0, int lane) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+          f[b][h][kb] = Cp[((int64_t)((db0 + b) * 2 + h) * KB + kb) * 64 + lane];
+  }
+  __device__ void apply(const f32x16& v, int b, f32x16 (&s)[KB], int act) const {
+    stage2_bf16<KB>(v, f[b], s, act);
+  }
+};
+template <int KB>
+struct CFrags<TrF32, KB> {
+  uint4 f[2][KB][4];  // [db2][kb][q]
+  __device__ void load(const uint4* __restrict__ Cp, int db0, int lane) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          f[b][kb][q] = Cp[(((int64_t)(db0 + b) * KB + kb) * 4 + q) * 64 + lane];
+  }
+  __device__ void apply(const f32x16& v, int b, f32x16 (&s)[KB], int act) const {
+    stage2_f32<KB>(v, f[b], s, act);
+  }
+};
+
+struct LargeWs {
+  unsigned* counters;  // [ntiles]
+  float* part;         // [DS][N][K]
+};
+
+__host__ __device__ inline LargeWs large_ws(void* ws, int64_t ntiles) {
+  LargeWs w;
+  w.counters = reinterpret_cast<unsigned*>(ws);
+  const size_t cbytes = ((size_t)ntiles * sizeof(unsigned) + 255) / 256 * 256;
+  w.part = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + cbytes);
+  return w;
+}
+
+// ---------------------------------------------------------------------------
+// The fused kernel.
+// ---------------------------------------------------------------------------
+template <class Tr, int NTILES, int KB>
+__global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
+    const typename Tr::elem* __restrict__ X, const uint4* __restrict__ Bp,
+    const uint4* __restrict__ Cp, int32_t* __restrict__ labels, float* __restrict__ scores,
+    int N, int F, int K, int ndb, int DS, int act, void* __restrict__ workspace) {
+  typedef typename Tr::elem T;
+  constexpr int NT = 32 * NTILES;
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nfs = nfs_of<Tr>(F);
+  const int pitch = pitch_of<Tr>(F);  // elements
+  const int ntiles = (int)cdiv(N, NT);
+  // Consecutive workgroups take different D slices, so with round-robin
+  // dispatch over the XCDs each XCD's L2 serves one slice of B.
+  const int slice = blockIdx.x % DS;
+  const int tile = blockIdx.x / DS;
+  const int n0 = tile * NT;
+  const int units = ndb / 2;
+  const int u_begin = (int)((int64_t)units * slice / DS);
+  const int u_end = (int)((int64_t)units * (slice + 1) / DS);
+
+  // ---- X tile -> LDS (rows n0..n0+NT, zero padded) -------------------------
+  T* xt = reinterpret_cast<T*>(lds);
+  {
+    // zero the padding columns F..nfs*kFStep and whole rows past N
+    const int fpad = nfs * Tr::kFStep;
+    for (int i = tid; i < NT * (fpad - F); i += kThreads) {
+      const int r = i / (fpad - F), c = F + i % (fpad - F);
+      xt[r * pitch + Tr::lds_pos(c)] = T(0);
+    }
+    const int rows = min(NT, N - n0);
+    for (int i = tid; i < (NT - rows) * fpad; i += kThreads) {
+      const int r = rows + i / fpad, c = i % fpad;
+      xt[r * pitch + Tr::lds_pos(c)] = T(0);
+    }
+    // The tile's rows are one contiguous range of X: read it with aligned
+    // 16-byte buffer loads (out-of-range dwords read as zero) and scatter.
+    const int64_t e0 = (int64_t)n0 * F, e1 = (int64_t)(n0 + rows) * F;
+    const int64_t g0 = e0 / Tr::kVec, g1 = cdiv(e1, Tr::kVec);
+    const T* base = X + g0 * Tr::kVec;
+    const int64_t total_bytes = ((int64_t)N * F - g0 * Tr::kVec) * Tr::kEsz;
+    const int nrec = (int)(total_bytes < 0x7fffffff ? total_bytes : 0x7fffffff);
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(base), 0, nrec, 0x00020000);
+    const int ng = (int)(g1 - g0);
+    const int64_t nx_total = (int64_t)N * F;
+    for (int g = tid; g < ng; g += kThreads) {
+      uint4 w;
+      if ((g0 + g + 1) * Tr::kVec <= nx_total) {
+        w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, g * 16, 0, 0));
+      } else {
+        // last, partial group of X: element loads inside the allocation only
+        uint32_t t[4] = {0u, 0u, 0u, 0u};
+        const int64_t first = (g0 + g) * Tr::kVec;
+        for (int j = 0; j < Tr::kVec; ++j) {
+          if (first + j >= nx_total) break;
+          if constexpr (Tr::kEsz == 2)
+            t[j >> 1] |= (uint32_t)X[first + j] << (16 * (j & 1));
+          else
+            t[j] = __float_as_uint(X[first + j]);
+        }
+        w = make_uint4(t[0], t[1], t[2], t[3]);
+      }
+      int64_t e = (g0 + g) * Tr::kVec - e0;  // element offset inside the tile
+      int r = (int)(e >= 0 ? e / F : -1);
+      int c = (int)(e - (int64_t)r * F);
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int j = 0; j < Tr::kVec; ++j) {
+        if (e >= 0 && r < rows) {
+          T val;
+          if constexpr (Tr::kEsz == 2) {
+            val = (uint16_t)(ws[j >> 1] >> (16 * (j & 1)));
+          } else {
+            val = __uint_as_float(ws[j]);
+          }
+          xt[r * pitch + Tr::lds_pos(c)] = val;
+        }
+        ++e;
+        if (e == 0) {
+          r = 0;
+          c = 0;
+        } else if (e > 0) {
+          if (++c == F) {
+            c = 0;
+            ++r;
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- main sweep over this wave's 64-dim units ---------------------------
+  f32x16 sacc[NTILES][KB];
+#pragma unroll
+  for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[t][kb][r] = 0.0f;
+
+  // byte offset of this lane's 16-byte X fragment word for f-step 0, tile 0
+  const int xrow = lane & 31, xhalf = lane >> 5;
+  const T* xlane = xt + xrow * pitch + xhalf * (Tr::kFStep / 2);
+  const int nfsl = (nfs + kPrefetch - 1) / kPrefetch * kPrefetch;
+
+  int u = u_begin + wave;
+  uint4 afr[kPrefetch][2];
+  auto bfrag = [&](int uu, int fs, int b) -> uint4 {
+    return Bp[((int64_t)(2 * uu + b) * nfs + fs) * 64 + lane];
+  };
+  if (u < u_end) {
+#pragma unroll
+    for (int i = 0; i < kPrefetch; ++i)
+      if (i < nfs) {
+        afr[i][0] = bfrag(u, i, 0);
+        afr[i][1] = bfrag(u, i, 1);
+      }
+  }
+  for (; u < u_end; u += kWaves) {
+    const int un = u + kWaves;
+    const bool has_next = un < u_end;
+    CFrags<Tr, KB> cf;
+    cf.load(Cp, 2 * u, lane);
+    f32x16 vacc[2][NTILES];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) vacc[b][t][r] = 0.0f;
+
+    uint4 xfr[2][NTILES];
+#pragma unroll
+    for (int t = 0; t < NTILES; ++t)
+      xfr[0][t] = *reinterpret_cast<const uint4*>(xlane + t * 32 * pitch);
+
+    for (int fs0 = 0; fs0 < nfsl; fs0 += kPrefetch) {
+#pragma unroll
+      for (int i = 0; i < kPrefetch; ++i) {
+        const int fs = fs0 + i;
+        if (fs < nfs) {
+          if (fs + 1 < nfs) {
+#pragma unroll
+            for (int t = 0; t < NTILES; ++t)
+              xfr[(i + 1) & 1][t] = *reinterpret_cast<const uint4*>(
+                  xlane + t * 32 * pitch + (fs + 1) * Tr::kFStep);
+          }
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
+        }
+        const int nx = fs + kPrefetch;
+        if (nx < nfs) {
+          afr[i][0] = bfrag(u, nx, 0);
+          afr[i][1] = bfrag(u, nx, 1);
+        } else if (has_next) {
+          const int j = nx - nfsl;
+          if (j >= 0 && j < nfs) {
+            afr[i][0] = bfrag(un, j, 0);
+            afr[i][1] = bfrag(un, j, 1);
+          }
+        }
+      }
+    }
+    // Stage II on the finished unit.
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t) cf.apply(vacc[b][t], b, sacc[t], act);
+  }
+
+  // ---- combine the waves' partial scores through LDS -----------------------
+  __syncthreads();  // X tile no longer needed
+  float* sred = reinterpret_cast<float*>(lds);  // [kWaves][NT][32*KB]
+  constexpr int KP = 32 * KB;
+#pragma unroll
+  for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int k = 32 * kb + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int n = 32 * t + (lane & 31);
+        sred[((int64_t)wave * NT + n) * KP + k] = sacc[t][kb][r];
+      }
+  __syncthreads();
+  const int rows = min(NT, N - n0);
+  if (DS == 1) {
+    for (int n = tid; n < rows; n += kThreads) {
+      float best = 0.0f;
+      int best_k = 0;
+      for (int k = 0; k < K; ++k) {
+        float s = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) s += sred[((int64_t)w * NT + n) * KP + k];
+        if (scores) scores[(int64_t)(n0 + n) * K + k] = s;
+        if (k == 0 || s > best) {
+          best = s;
+          best_k = k;
+        }
+      }
+      labels[n0 + n] = best_k;
+    }
+    return;
+  }
+  // Split-D: publish this slice's partial, the last slice of the tile finishes.
+  const LargeWs ws = large_ws(workspace, ntiles);
+  float* mypart = ws.part + (int64_t)slice * N * K;
+  for (int i = tid; i < rows * K; i += kThreads) {
+    const int n = i / K, k = i - n * K;
+    float s = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += sred[((int64_t)w * NT + n) * KP + k];
+    mypart[(int64_t)(n0 + n) * K + k] = s;
+  }
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) s_last = (atomicAdd(ws.counters + tile, 1u) == (unsigned)DS - 1) ? 1 : 0;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  for (int n = tid; n < rows; n += kThreads) {
+    float best = 0.0f;
+    int best_k = 0;
+    for (int k = 0; k < K; ++k) {
+      float s = 0.0f;
+      for (int sl = 0; sl < DS; ++sl)
+        s += load_coherent(ws.part + ((int64_t)sl * N + n0 + n) * K + k);
+      if (scores) scores[(int64_t)(n0 + n) * K + k] = s;
+      if (k == 0 || s > best) {
+        best = s;
+        best_k = k;
+      }
+    }
+    labels[n0 + n] = best_k;
+  }
+  if (tid == 0)
+    __hip_atomic_store(ws.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
+// Host-side configuration.
+// ---------------------------------------------------------------------------
+struct LargeCfg {
+  int ntiles_per_wg;  // NTILES
+  int kb;
+  int ds;
+  int64_t ntiles;      // sample tiles
+  size_t lds;
+  bool ok;
+};
+
+template <class Tr>
+LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
+  LargeCfg c{};
+  if (cdiv(K, 32) > 4 || F > (1 << 20) || N > (1 << 30)) return c;
+  const int pitch = pitch_of<Tr>((int)F);
+  const int kbr = kb_of(K);
+  for (int nt : {4, 2, 1}) {
+    if (nt == 4 && kbr > 2) continue;
+    const size_t xbytes = (size_t)32 * nt * pitch * Tr::kEsz;
+    const size_t rbytes = (size_t)kWaves * 32 * nt * 32 * kbr * 4;
+    const size_t need = xbytes > rbytes ? xbytes : rbytes;
+    if (need <= (size_t)kLdsBytes) {
+      c.ntiles_per_wg = nt;
+      c.lds = need;
+      break;
+    }
+  }
+  if (!c.ntiles_per_wg) return c;
+  c.kb = kbr;
+  c.ntiles = cdiv(N, 32 * c.ntiles_per_wg);
+  // Split D when there are too few sample tiles to give every CU a workgroup.
+  const int64_t units = cdiv(D, 64);
+  int ds = 1;
+  while (c.ntiles * ds < 256 && ds < 16 && units / (ds * 2) >= kWaves) ds *= 2;
+  c.ds = ds;
+  c.ok = true;
+  return c;
+}
+
+template <class Tr, int NTILES, int KB>
+hipError_t launch_cfg(const LargeCfg& c, const void* X, const uint4* Bp, const uint4* Cp,
+                      int32_t* labels, float* scores, int64_t N, int64_t F, int64_t K, int ndb,
+                      int act, void* ws, hipStream_t stream) {
+  const dim3 grid((unsigned)(c.ntiles * c.ds)), block(kThreads);
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&large_fused_kernel<Tr, NTILES, KB>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((large_fused_kernel<Tr, NTILES, KB>), grid, block, c.lds, stream,
+                     (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F, (int)K,
+                     ndb, c.ds, act, ws);
+  return hipGetLastError();
+}
+
+template <class Tr>
+hipError_t launch_tr(const void* X, const void* packed, int32_t* labels, float* scores,
+                     int64_t N, int64_t F, int64_t D, int64_t K, int act, void* ws,
+                     hipStream_t stream) {
+  const LargeCfg c = large_cfg<Tr>(N, F, D, K);
+  if (!c.ok) return hipErrorInvalidValue;
+  const PackGeom g = pack_geom<Tr>(F, D, K);
+  const uint4* Bp = (const uint4*)packed;
+  const uint4* Cp = (const uint4*)((const char*)packed + g.b_bytes);
+  const int nt = c.ntiles_per_wg, kb = c.kb;
+#define HD_LAUNCH(NTV, KBV)                                                                       \
+  if (nt == NTV && kb == KBV)                                                                     \
+    return launch_cfg<Tr, NTV, KBV>(c, X, Bp, Cp, labels, scores, N, F, K, g.ndb, act, ws, stream);
+  HD_LAUNCH(4, 1)
+  HD_LAUNCH(4, 2)
+  HD_LAUNCH(2, 1)
+  HD_LAUNCH(2, 2)
+  HD_LAUNCH(2, 4)
+  HD_LAUNCH(1, 1)
+  HD_LAUNCH(1, 2)
+  HD_LAUNCH(1, 4)
+#undef HD_LAUNCH
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool large_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  return dt == 0 ? large_cfg<TrF32>(N, F, D, K).ok : large_cfg<TrBF16>(N, F, D, K).ok;
+}
+
+size_t large_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {
+  const PackGeom g = dt == 0 ? pack_geom<TrF32>(F, D, K) : pack_geom<TrBF16>(F, D, K);
+  return g.b_bytes + g.c_bytes;
+}
+
+size_t large_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  const LargeCfg c = dt == 0 ? large_cfg<TrF32>(N, F, D, K) : large_cfg<TrBF16>(N, F, D, K);
+  if (!c.ok || c.ds == 1) return 0;
+  const size_t cbytes = ((size_t)c.ntiles * sizeof(unsigned) + 255) / 256 * 256;
+  return cbytes + sizeof(float) * (size_t)c.ds * N * K;
+}
+
+hipError_t launch_pack(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,
+                       void* packed, hipStream_t stream) {
+  if (dt == 0) {
+    const PackGeom g = pack_geom<TrF32>(F, D, K);
+    uint4* Bp = (uint4*)packed;
+    uint4* Cp = (uint4*)((char*)packed + g.b_bytes);
+    hipLaunchKernelGGL(pack_b_f32, dim3((unsigned)((int64_t)g.ndb * g.nfs)), dim3(64), 0, stream,
+                       (const float*)B, Bp, (int)F, (int)D, g.ndb, g.nfs);
+    hipLaunchKernelGGL(pack_c_f32, dim3((unsigned)((int64_t)g.ndb * g.kb * 4)), dim3(64), 0,
+                       stream, (const float*)C, Cp, (int)D, (int)K, g.ndb, g.kb);
+  } else {
+    const PackGeom g = pack_geom<TrBF16>(F, D, K);
+    uint4* Bp = (uint4*)packed;
+    uint4* Cp = (uint4*)((char*)packed + g.b_bytes);
+    hipLaunchKernelGGL(pack_b_bf16, dim3((unsigned)((int64_t)g.ndb * g.nfs)), dim3(64), 0,
+                       stream, (const bf16raw*)B, Bp, (int)F, (int)D, g.ndb, g.nfs);
+    hipLaunchKernelGGL(pack_c_bf16, dim3((unsigned)((int64_t)g.ndb * 2 * g.kb)), dim3(64), 0,
+                       stream, (const bf16raw*)C, Cp, (int)D, (int)K, g.ndb, g.kb);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_large(const void* X, const void* packed, int32_t* labels, float* scores,
+                        int64_t N, int64_t F, int64_t D, int64_t K, int dt, int act,
+                        void* workspace, hipStream_t stream) {
+  if (dt == 0)
+    return launch_tr<TrF32>(X, packed, labels, scores, N, F, D, K, act, workspace, stream);
+  return launch_tr<TrBF16>(X, packed, labels, scores, N, F, D, K, act, workspace, stream);
+}
+
+}  // namespace hd

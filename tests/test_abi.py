@@ -1,0 +1,102 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+``include/hd.h`` declares, and rejects bad arguments on the host before any
+HIP call (these calls return before anything is enqueued)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2506_09282_amd as hd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hd.h")
+FAKE = 0x10000  # never dereferenced: validation fails first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hd_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(hd.LIB_PATH):
+        from paper_2506_09282_amd import build
+        build.build()
+    return hd.lib()
+
+
+def test_header_symbols_exported(L):
+    names = declared_functions()
+    assert set(names) == set(hd.SYMBOLS), names
+    raw = ctypes.CDLL(hd.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+def test_status_strings(L):
+    for s in range(5):
+        assert L.hd_status_str(s).startswith(b"HD_")
+    assert L.hd_status_str(99) == b"HD_ERR_UNKNOWN"
+
+
+def test_workspace_sizes(L):
+    # small batch: 256-byte ticket header + replicated accumulators
+    small = L.hd_infer_workspace_bytes(32, 561, 10240, 6, hd.HD_F32)
+    assert small == 256 + 4 * 32 * 32 * 6
+    assert L.hd_infer_workspace_bytes(0, 561, 10240, 6, hd.HD_F32) == 0
+    assert L.hd_infer_workspace_bytes(5, 0, 10, 6, hd.HD_F32) == 0
+    # large batch, raw entry: holds the tiled model
+    big = L.hd_infer_workspace_bytes(65536, 617, 10240, 26, hd.HD_BF16)
+    tiled_b = 320 * 39 * 1024
+    assert big >= tiled_b
+    assert L.hd_infer_packed_workspace_bytes(65536, 617, 10240, 26, hd.HD_BF16) < tiled_b
+    img = L.hd_model_packed_bytes(617, 10240, 26, hd.HD_BF16)
+    assert img >= tiled_b + 617 * 10240 * 2 + 26 * 10240 * 2
+
+
+def _infer(L, X=FAKE, B=FAKE, C=FAKE, labels=FAKE, scores=None, N=4, F=8, D=64, K=3,
+           dt=hd.HD_F32, act=0, ws=FAKE, wsb=1 << 20):
+    return L.hd_infer(X, B, C, labels, scores, N, F, D, K, dt, act, ws, wsb, None)
+
+
+def test_infer_argument_errors(L):
+    assert _infer(L, X=None) == hd.HD_ERR_ARG
+    assert _infer(L, B=None) == hd.HD_ERR_ARG
+    assert _infer(L, C=None) == hd.HD_ERR_ARG
+    assert _infer(L, labels=None) == hd.HD_ERR_ARG
+    assert _infer(L, N=-1) == hd.HD_ERR_ARG
+    assert _infer(L, F=0) == hd.HD_ERR_ARG
+    assert _infer(L, D=0) == hd.HD_ERR_ARG
+    assert _infer(L, K=0) == hd.HD_ERR_ARG
+    assert _infer(L, dt=7) == hd.HD_ERR_ARG
+    assert _infer(L, act=5) == hd.HD_ERR_ARG
+    assert _infer(L, ws=None) == hd.HD_ERR_ARG
+    assert _infer(L, wsb=16) == hd.HD_ERR_WORKSPACE
+    assert _infer(L, F=1 << 31) == hd.HD_ERR_UNSUPPORTED
+    # N == 0 is a no-op, even with null buffers
+    assert _infer(L, N=0, X=None, labels=None, ws=None, wsb=0) == hd.HD_OK
+
+
+def test_other_entry_argument_errors(L):
+    assert L.hd_encode(None, FAKE, FAKE, 4, 8, 16, 0, 0, None) == hd.HD_ERR_ARG
+    assert L.hd_encode(FAKE, FAKE, FAKE, 4, 0, 16, 0, 0, None) == hd.HD_ERR_ARG
+    assert L.hd_encode(FAKE, FAKE, FAKE, 0, 8, 16, 0, 0, None) == hd.HD_OK
+    assert L.hd_similarity(FAKE, None, FAKE, None, 4, 16, 3, 0, None) == hd.HD_ERR_ARG
+    assert L.hd_similarity(FAKE, FAKE, FAKE, None, 4, 16, 0, 0, None) == hd.HD_ERR_ARG
+    assert L.hd_pack_model(FAKE, FAKE, 8, 16, 3, 0, FAKE, 8, None) == hd.HD_ERR_WORKSPACE
+    assert L.hd_pack_model(None, FAKE, 8, 16, 3, 0, FAKE, 1 << 30, None) == hd.HD_ERR_ARG
+    assert L.hd_infer_packed(FAKE, None, FAKE, None, 100, 8, 16, 3, 0, 0, FAKE, 1 << 20,
+                             None) == hd.HD_ERR_ARG
+
+
+def test_product_path_does_not_touch_oracle():
+    """The binding and the HIP sources never import, link or load the oracle."""
+    pkg = os.path.join(ROOT, "paper_2506_09282_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.lower(), f

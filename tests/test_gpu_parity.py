@@ -1,0 +1,211 @@
+"""GPU parity: the HIP path (called through the C ABI) against the oracle.
+
+Scores agree within 1e-4 of ||c_k||_1 plus the fragile-set allowance, labels
+agree except where the oracle's margin lies inside the allowances (see
+tolerance.py); on small-integer inputs every summation order is exact, so
+there scores and labels must be bit-identical.
+"""
+import numpy as np
+import pytest
+
+import hd_inputs
+import oracle
+from gpu_util import BF16_DRIFT, RTOL, announce, check_against_oracle, dev, torch_or_skip
+from tolerance import compare
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def hd():
+    torch_or_skip()
+    import paper_2506_09282_amd as hd
+    hd.lib()  # raise now if the library is missing
+    return hd
+
+
+def run(hd, X, B, C, dtype, act="hardsign", scores=True, packed=False):
+    torch = torch_or_skip()
+    Xd, Bd, Cd = dev(X, dtype), dev(B, dtype), dev(C, dtype)
+    if packed:
+        model = hd.pack_model(Bd, Cd)
+        out = hd.infer_packed(Xd, model, act=act, return_scores=scores)
+    else:
+        out = hd.infer(Xd, Bd, Cd, act=act, return_scores=scores)
+    torch.cuda.synchronize()
+    if scores:
+        y, S = out
+        return y.cpu().numpy(), S.cpu().numpy().astype(np.float64)
+    return out.cpu().numpy(), None
+
+
+def inputs(N, F, D, K, dist="uniform_pm1", seed=0, dtype="f32"):
+    return hd_inputs.make_inputs(N, F, D, K, dist, seed=seed, dtype=dtype)
+
+
+# --- the named workloads ----------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tiny_workload(hd, dtype):
+    w = hd_inputs.WORKLOADS["tiny"]
+    announce(f"tiny {dtype}")
+    X, B, C = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype=dtype)
+    y, S = run(hd, X, B, C, dtype)
+    rep, _ = check_against_oracle(X, B, C, y, S)
+    assert rep["ok"], rep
+
+
+@pytest.mark.parametrize("name", ["activity_n1", "activity_n32"])
+def test_activity_workloads(hd, name):
+    w = hd_inputs.WORKLOADS[name]
+    announce(name)
+    X, B, C = inputs(w.N, w.F, w.D, w.K, w.x_dist)
+    y, S = run(hd, X, B, C, "f32")
+    rep, _ = check_against_oracle(X, B, C, y, S)
+    assert rep["ok"], rep
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_image_workload_sampled(hd, dtype):
+    w = hd_inputs.WORKLOADS["image"]
+    announce(f"image {dtype}")
+    X, B, C = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype=dtype)
+    y, S = run(hd, X, B, C, dtype)
+    rows = np.r_[0:40, w.N - 40:w.N, np.random.default_rng(1).integers(0, w.N, 48)]
+    rep, _ = check_against_oracle(X, B, C, y, S, rows=rows)
+    assert rep["ok"], rep
+
+
+def test_speech_workload_sampled(hd):
+    w = hd_inputs.WORKLOADS["speech"]
+    announce("speech bf16 N=65536")
+    X, B, C = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype="bf16")
+    y, S = run(hd, X, B, C, "bf16")
+    rows = np.r_[0:32, 4090:4100, w.N - 32:w.N, np.random.default_rng(2).integers(0, w.N, 64)]
+    rep, _ = check_against_oracle(X, B, C, y, S, rows=rows)
+    assert rep["ok"], rep
+    # drift of the bf16 path against the fp32-input oracle
+    X32, B32, C32 = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype="f32")
+    ref32 = oracle.infer(X32, B32, C32, rows=rows)
+    c1 = np.abs(C32.astype(np.float64)).sum(axis=1)
+    drift = np.abs(S[rows] - ref32["S"]) / c1[None, :]
+    assert drift.max() <= BF16_DRIFT, drift.max()
+
+
+# --- exactness on small-integer inputs --------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,F,D,K", [(1, 561, 10240, 6), (32, 33, 1000, 5), (64, 100, 2048, 17),
+                                     (65, 100, 2048, 17), (300, 617, 4096, 26),
+                                     (257, 31, 700, 3)])
+def test_integer_inputs_bit_exact(hd, dtype, N, F, D, K):
+    announce(f"integer {dtype} N={N} F={F} D={D} K={K}")
+    X, B, C = hd_inputs.make_integer_inputs(N, F, D, K, seed=N + F)
+    y, S = run(hd, X, B, C, dtype)
+    ref = oracle.infer(X, B, C)
+    assert np.array_equal(S, ref["S"]), np.abs(S - ref["S"]).max()
+    assert np.array_equal(y, ref["y"])
+
+
+@pytest.mark.parametrize("N", [5, 200])
+def test_hardsign_zero_and_argmax_ties(hd, N):
+    """Inputs in {-1, 0, 1}: many v = 0 (HardSign ties to +1) and duplicated
+    class rows (argmax ties to the lowest index)."""
+    announce(f"ties N={N}")
+    X, B, C = hd_inputs.make_integer_inputs(N, 40, 512, 4, seed=3, x_range=1, b_range=1)
+    C = np.vstack([C, C[1:2], C[0:1]])
+    for dtype in ("f32", "bf16"):
+        y, S = run(hd, X, B, C, dtype)
+        ref = oracle.infer(X, B, C, want_va=True)
+        assert (ref["V"] == 0).any()
+        assert np.array_equal(S, ref["S"]) and np.array_equal(y, ref["y"])
+
+
+# --- edge shapes --------------------------------------------------------------
+
+EDGE = [(1, 1, 1, 1), (2, 2, 7, 2), (3, 5, 33, 1), (31, 17, 2047, 2), (33, 64, 10000, 6),
+        (63, 1, 96, 3), (64, 561, 2048, 6), (65, 31, 100, 17), (100, 33, 1000, 33),
+        (129, 200, 640, 100), (300, 16, 64, 64), (1000, 7, 129, 9)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,F,D,K", EDGE)
+def test_edge_shapes(hd, dtype, N, F, D, K):
+    announce(f"edge {dtype} N={N} F={F} D={D} K={K}")
+    X, B, C = inputs(N, F, D, K, "normal", seed=N * 7 + D, dtype=dtype)
+    y, S = run(hd, X, B, C, dtype)
+    rep, _ = check_against_oracle(X, B, C, y, S)
+    assert rep["ok"], rep
+
+
+def test_empty_batch(hd):
+    torch = torch_or_skip()
+    X = torch.empty((0, 10), device="cuda")
+    B = torch.randn(10, 64, device="cuda")
+    C = torch.randn(3, 64, device="cuda")
+    y = hd.infer(X, B, C)
+    assert y.shape == (0,)
+
+
+@pytest.mark.parametrize("N", [16, 500])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_identity_activation(hd, N, dtype):
+    announce(f"identity {dtype} N={N}")
+    X, B, C = inputs(N, 50, 777, 5, "normal", seed=4, dtype=dtype)
+    y, S = run(hd, X, B, C, dtype, act="identity")
+    rep, _ = check_against_oracle(X, B, C, y, S, act="identity")
+    assert rep["ok"], rep
+
+
+@pytest.mark.parametrize("N", [8, 300])
+def test_labels_without_scores_and_repeat(hd, N):
+    """scores = NULL writes labels only; repeated calls on one workspace
+    (self-cleaning accumulators and tickets) give the same labels."""
+    announce(f"no-scores N={N}")
+    X, B, C = inputs(N, 61, 3000, 7, seed=5)
+    y0, _ = run(hd, X, B, C, "f32", scores=False)
+    ref = oracle.infer(X, B, C, want_va=True)
+    rep = compare(None, y0, ref, C, 61, RTOL)
+    assert rep["ok"], rep
+    for _ in range(5):
+        y1, _ = run(hd, X, B, C, "f32", scores=False)
+        assert np.array_equal(y0, y1)
+
+
+@pytest.mark.parametrize("N", [4, 1000])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_packed_model_matches_raw(hd, N, dtype):
+    announce(f"packed {dtype} N={N}")
+    X, B, C = inputs(N, 99, 2000, 12, seed=6, dtype=dtype)
+    y0, S0 = run(hd, X, B, C, dtype)
+    y1, S1 = run(hd, X, B, C, dtype, packed=True)
+    assert np.array_equal(y0, y1)
+    assert np.array_equal(S0, S1)
+
+
+# --- the stages alone -----------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_encode_then_similarity(hd, dtype):
+    torch = torch_or_skip()
+    announce(f"encode/similarity {dtype}")
+    X, B, C = inputs(70, 120, 1500, 9, seed=7, dtype=dtype)
+    Xd, Bd, Cd = dev(X, dtype), dev(B, dtype), dev(C, dtype)
+    H = hd.encode(Xd, Bd)
+    y, S = hd.similarity(H, Cd, return_scores=True)
+    torch.cuda.synchronize()
+    ref = oracle.infer(X, B, C, want_va=True)
+    from tolerance import encode_allowed_mismatch
+    ok, bad, flips = encode_allowed_mismatch(H.cpu().numpy(), ref, 120)
+    assert ok, (bad, flips)
+    rep = compare(S.cpu().numpy(), y.cpu().numpy(), ref, C, 120, RTOL)
+    assert rep["ok"], rep
+    # Stage II alone on the GPU's own H against the oracle's Stage II on it
+    Hn = H.cpu().numpy().astype(np.float64)
+    r2 = oracle.similarity(Hn, C)
+    c1 = np.abs(C.astype(np.float64)).sum(axis=1)
+    assert np.all(np.abs(S.cpu().numpy() - r2["S"]) <= RTOL * c1[None, :])
+    # identity encoding
+    Hi = hd.encode(Xd, Bd, act="identity").cpu().numpy()
+    ok, bad, _ = encode_allowed_mismatch(Hi, ref, 120, act="identity")
+    assert ok, bad
