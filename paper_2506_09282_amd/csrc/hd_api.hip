@@ -15,7 +15,11 @@ bool enums_ok(int dt, int act) { return (dt == HD_F32 || dt == HD_BF16) && (act 
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-bool use_small(int64_t N) { return N <= hd::kSmallMaxN; }
+// The split-D small-batch path serves N <= 64 whenever its scratch fits;
+// everything else takes the batch-split matrix-core path.
+bool use_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  return N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt);
+}
 
 hd_status from_hip(hipError_t e) { return e == hipSuccess ? HD_OK : HD_ERR_HIP; }
 
@@ -82,13 +86,13 @@ size_t hd_model_packed_bytes(int64_t F, int64_t D, int64_t K, hd_dtype dt) {
 
 size_t hd_infer_packed_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
   if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
-  if (use_small(N)) return hd::small_workspace_bytes(N, F, D, K);
+  if (use_small(N, F, D, K, dt)) return hd::small_workspace_bytes(N, F, D, K, dt);
   return hd::large_workspace_bytes(N, F, D, K, dt);
 }
 
 size_t hd_infer_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
   if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
-  if (use_small(N)) return hd::small_workspace_bytes(N, F, D, K);
+  if (use_small(N, F, D, K, dt)) return hd::small_workspace_bytes(N, F, D, K, dt);
   return align256(hd::large_packed_bytes(F, D, K, dt)) +
          hd::large_workspace_bytes(N, F, D, K, dt);
 }
@@ -119,7 +123,7 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
   if (!dims_ok(N, F, D, K)) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!X || !labels || (packed ? false : (!B || !C))) return HD_ERR_ARG;
-  const bool small = use_small(N);
+  const bool small = use_small(N, F, D, K, dt);
   if (!small && !hd::large_supported(N, F, D, K, dt)) return HD_ERR_UNSUPPORTED;
   const size_t need = packed ? hd_infer_packed_workspace_bytes(N, F, D, K, dt)
                              : hd_infer_workspace_bytes(N, F, D, K, dt);

@@ -47,13 +47,34 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Loads that must observe other workgroups' device-scope atomics/stores
-// made before a release/acquire handshake.
-__device__ __forceinline__ float load_coherent(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Cross-workgroup hand-off without cache write-back.
+//
+// Data that one workgroup passes to another moves only through device-scope
+// atomic read-modify-writes, which are performed at a single coherence point
+// for each address. A workgroup publishes with no-return atomics, waits until
+// they are performed (s_waitcnt, all counters to zero) and only then takes a
+// ticket with a relaxed device-scope fetch-add; the workgroup that draws the
+// last ticket reads every published value with an atomic exchange against 0,
+// which both observes all performed atomics and leaves the slot zeroed for
+// the next call. A device-scope release fence would also work, but on gfx950
+// it writes back the whole L2 (buffer_wbl2) in every workgroup, which costs
+// tens of microseconds per launch.
+__device__ __forceinline__ void wait_own_memory_ops() { __builtin_amdgcn_s_waitcnt(0); }
+__device__ __forceinline__ unsigned take_ticket(unsigned* counter) {
+  return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void store_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ float take_and_clear(float* p) {
+  return __hip_atomic_exchange(p, 0.0f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void publish_add(float* p, float v) {
+  unsafeAtomicAdd(p, v);  // native no-return fp32 atomic add (device memory)
+}
+__device__ __forceinline__ void publish_store(float* p, float v) {
+  // an exchange (not a plain store) so the value lands where atomics are performed
+  (void)__hip_atomic_exchange(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void reset_counter(unsigned* counter) {
+  (void)__hip_atomic_exchange(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __host__ __device__ constexpr int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }

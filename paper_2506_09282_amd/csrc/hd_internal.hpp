@@ -9,10 +9,10 @@ namespace hd {
 
 // Small-batch fused path (split-D across workgroups).
 constexpr int kSmallMaxN = 64;
-constexpr int kSmallCols = 32;   // hypervector columns per workgroup
-constexpr int kSmallReplicas = 32;
+constexpr int kSmallReplicas = 32;  // replicated score accumulators
 
-size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K);
+bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
+size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 hipError_t launch_small(const void* X, const void* B, const void* C, int32_t* labels,
                         float* scores, int64_t N, int64_t F, int64_t D, int64_t K, int dt,
                         int act, void* workspace, hipStream_t stream);

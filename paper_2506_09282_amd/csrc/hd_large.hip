@@ -35,6 +35,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kPrefetch = 4;  // f-steps of B fragments in flight per wave
+constexpr int kMaxSlices = 16;  // D slices per sample tile (split-D)
 constexpr int kLdsBytes = 160 * 1024 - 256;  // leave room for static LDS
 
 template <typename U, typename V>
@@ -476,33 +477,34 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     for (int t = 0; t < NTILES; ++t)
       xfr[0][t] = *reinterpret_cast<const uint4*>(xlane + t * 32 * pitch);
 
+    // Every step issues the same loads unconditionally (addresses clamped to
+    // valid fragments) so the hardware wait counters can be tracked across
+    // the loop; only the memory-free MFMA block is predicated.
     for (int fs0 = 0; fs0 < nfsl; fs0 += kPrefetch) {
 #pragma unroll
       for (int i = 0; i < kPrefetch; ++i) {
         const int fs = fs0 + i;
-        if (fs < nfs) {
-          if (fs + 1 < nfs) {
+        const int fsn = min(fs + 1, nfs - 1);
 #pragma unroll
-            for (int t = 0; t < NTILES; ++t)
-              xfr[(i + 1) & 1][t] = *reinterpret_cast<const uint4*>(
-                  xlane + t * 32 * pitch + (fs + 1) * Tr::kFStep);
-          }
+        for (int t = 0; t < NTILES; ++t)
+          xfr[(i + 1) & 1][t] =
+              *reinterpret_cast<const uint4*>(xlane + t * 32 * pitch + fsn * Tr::kFStep);
+        if (fs < nfs) {
 #pragma unroll
           for (int b = 0; b < 2; ++b)
 #pragma unroll
             for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
         }
+        // ring refill: step fs + kPrefetch of this unit, else the first steps
+        // of the wave's next unit, else a harmless reload of a valid fragment
         const int nx = fs + kPrefetch;
-        if (nx < nfs) {
-          afr[i][0] = bfrag(u, nx, 0);
-          afr[i][1] = bfrag(u, nx, 1);
-        } else if (has_next) {
-          const int j = nx - nfsl;
-          if (j >= 0 && j < nfs) {
-            afr[i][0] = bfrag(un, j, 0);
-            afr[i][1] = bfrag(un, j, 1);
-          }
-        }
+        const int j = nx - nfsl;
+        const bool cur = nx < nfs;
+        const bool nxt = !cur && has_next && j >= 0 && j < nfs;
+        const int tu = nxt ? un : u;
+        const int tf = cur ? nx : (nxt ? j : nfs - 1);
+        afr[i][0] = bfrag(tu, tf, 0);
+        afr[i][1] = bfrag(tu, tf, 1);
       }
     }
     // Stage II on the finished unit.
@@ -546,7 +548,8 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     }
     return;
   }
-  // Split-D: publish this slice's partial, the last slice of the tile finishes.
+  // Split-D: publish this slice's partial, the last slice of the tile finishes
+  // (summing the slices in a fixed order, so results are deterministic).
   const LargeWs ws = large_ws(workspace, ntiles);
   float* mypart = ws.part + (int64_t)slice * N * K;
   for (int i = tid; i < rows * K; i += kThreads) {
@@ -554,21 +557,30 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     float s = 0.0f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) s += sred[((int64_t)w * NT + n) * KP + k];
-    mypart[(int64_t)(n0 + n) * K + k] = s;
+    publish_store(mypart + (int64_t)(n0 + n) * K + k, s);
   }
-  __threadfence();
+  wait_own_memory_ops();
   __syncthreads();
-  if (tid == 0) s_last = (atomicAdd(ws.counters + tile, 1u) == (unsigned)DS - 1) ? 1 : 0;
+  if (tid == 0) s_last = (take_ticket(ws.counters + tile) == (unsigned)DS - 1) ? 1 : 0;
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
+  for (int i = tid; i < rows * K; i += kThreads) {
+    const int n = i / K, k = i - n * K;
+    float t[kMaxSlices];
+#pragma unroll
+    for (int sl = 0; sl < kMaxSlices; ++sl)
+      t[sl] = sl < DS ? take_and_clear(ws.part + ((int64_t)sl * N + n0 + n) * K + k) : 0.0f;
+    float s = 0.0f;
+#pragma unroll
+    for (int sl = 0; sl < kMaxSlices; ++sl) s += t[sl];
+    sred[i] = s;  // the per-wave partials are no longer needed
+  }
+  __syncthreads();
   for (int n = tid; n < rows; n += kThreads) {
     float best = 0.0f;
     int best_k = 0;
     for (int k = 0; k < K; ++k) {
-      float s = 0.0f;
-      for (int sl = 0; sl < DS; ++sl)
-        s += load_coherent(ws.part + ((int64_t)sl * N + n0 + n) * K + k);
+      const float s = sred[n * K + k];
       if (scores) scores[(int64_t)(n0 + n) * K + k] = s;
       if (k == 0 || s > best) {
         best = s;
@@ -577,8 +589,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     }
     labels[n0 + n] = best_k;
   }
-  if (tid == 0)
-    __hip_atomic_store(ws.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) reset_counter(ws.counters + tile);
 }
 
 // ---------------------------------------------------------------------------
@@ -616,7 +627,7 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
   // Split D when there are too few sample tiles to give every CU a workgroup.
   const int64_t units = cdiv(D, 64);
   int ds = 1;
-  while (c.ntiles * ds < 256 && ds < 16 && units / (ds * 2) >= kWaves) ds *= 2;
+  while (c.ntiles * ds < 256 && ds < kMaxSlices && units / (ds * 2) >= kWaves) ds *= 2;
   c.ds = ds;
   c.ok = true;
   return c;

@@ -2,15 +2,33 @@
 // small-batch variant (Sec. III-C, Alg. 3), which splits the hypervector
 // dimension D across workers and sums their partial score matrices.
 //
-// One workgroup owns 32 consecutive columns of B (a "column block" of the
-// encoded matrix, Alg. 2) and all F rows of it, so its encoding sums are
-// complete and HardSign (Eq. 1) is applied in registers: H never leaves the
-// chip. B is read exactly once, as coalesced 128-byte row segments (fp32).
-// Each workgroup then forms its partial S over its 32 columns and adds it,
-// with fp32 atomics, into one of R replicated accumulators (R spreads the
-// atomic traffic over many cache lines). The last workgroup to finish (an
-// atomic ticket) sums the replicas, takes the row argmax (Eq. 9), writes
-// labels/scores and re-zeroes the accumulators and the ticket.
+// Work unit. A "column block" is 16 consecutive columns of B with all F rows
+// (a column block of the encoded matrix, Alg. 2): its encoding sums are
+// complete inside one workgroup, so HardSign (Eq. 1) is applied on chip and H
+// never reaches device memory. B is read exactly once.
+//
+// Grid. One persistent workgroup per compute unit walks its share of column
+// blocks; the next block's B rows are in flight while the current block is
+// computed. Blocks are ordered so that each XCD (with its own L2) walks a
+// contiguous range of columns, so blocks sharing 128-byte L2 lines are read
+// through the same L2.
+//
+// Compute. N <= 8 (and bf16 inputs): plain fp32 FMAs. 8 < N <= 64 with fp32
+// inputs: the 16x16x4 fp32 matrix instruction (twice the unpacked vector FMA
+// rate), with X^T staged in LDS as the B operand and B's row segments as the
+// A operand.
+//
+// Reduction. Each workgroup sums its blocks' partial scores locally, adds
+// them with fp32 atomics into one of R replicated accumulators, and takes a
+// ticket; the last workgroup reads-and-clears the replicas, takes the row
+// argmax (Eq. 9) and writes labels/scores. hd_common.hpp explains why the
+// hand-off uses atomics and no device-scope fence.
+//
+// Wait counters. Global loads are issued unconditionally (addresses clamped
+// into the buffers, results selected afterwards) so the compiler can track
+// how many are outstanding across loop iterations; a block's C rows are loaded
+// before the next block's B rows, so waiting for them does not drain the
+// prefetch.
 #include "hd_common.hpp"
 #include "hd_internal.hpp"
 
@@ -19,15 +37,12 @@ namespace hd {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kColGroups = kSmallCols / 4;         // 8 groups of 4 columns
-constexpr int kRowGroups = kThreads / kColGroups;  // 32 row groups
-constexpr int kRowsPerBatch = 8;                   // B rows per thread per load batch
-constexpr int kXsFloats = 16384;                   // LDS budget for the staged X^T chunk
-
-template <int NB>
-constexpr int xs_pitch() {
-  return NB >= 4 ? NB + 4 : NB;
-}
+constexpr int kWaves = kThreads / kWave;
+constexpr int kW = 16;                // columns per block
+constexpr int kCG = kW / 4;           // float4 column groups per block
+constexpr int kRG = kThreads / kCG;   // row groups (VALU kernel)
+constexpr int kRpt = 12;              // B rows per thread per chunk (VALU kernel)
+constexpr int kLdsBudget = 159 * 1024;
 
 struct SmallWs {
   unsigned* counter;
@@ -41,218 +56,673 @@ __host__ __device__ inline SmallWs small_ws(void* ws) {
   return w;
 }
 
-template <typename T, bool VEC>
-__device__ __forceinline__ float4 load_b4(const T* __restrict__ B, int64_t row, int64_t col,
-                                          int64_t D) {
-  if (VEC) {
-    if (col < D) return load4(B, row * D + col);
-    return make_float4(0.f, 0.f, 0.f, 0.f);
+__host__ __device__ inline int replicas(int G) { return G < kSmallReplicas ? G : kSmallReplicas; }
+
+// Block order. Workgroups are dispatched round-robin over the 8 XCDs, so
+// workgroup b runs on XCD b % 8. The blocks are split evenly between XCDs
+// into contiguous ranges (neighbouring blocks share 128-byte L2 lines), and
+// each XCD's workgroups take its range round-robin. A workgroup's k-th block
+// is block_of(k); it owns blocks while block_of(k) < its XCD's range end.
+struct BlockWalk {
+  int start, stride, end;
+  __device__ int block_of(int k) const { return start + k * stride; }
+  __device__ int count() const { return start < end ? (end - start + stride - 1) / stride : 0; }
+};
+
+__device__ __forceinline__ BlockWalk block_walk(int b, int G, int nblocks) {
+  const int x = b % 8, j = b / 8;
+  const int per = G / 8, rem = G % 8;
+  const int gx = per + (x < rem ? 1 : 0);  // workgroups on this XCD
+  const int nx = G < 8 ? G : 8;            // XCDs that have workgroups
+  BlockWalk w;
+  if (x >= nx) {
+    w.start = w.end = 0;
+    w.stride = 1;
+    return w;
   }
+  const int r0 = (int)((int64_t)nblocks * x / nx), r1 = (int)((int64_t)nblocks * (x + 1) / nx);
+  w.start = r0 + j;
+  w.stride = gx;
+  w.end = r1;
+  return w;
+}
+
+template <typename T>
+__device__ __forceinline__ float4 load_b4_vec(const T* __restrict__ B, int64_t row, int64_t col,
+                                              int64_t D) {
+  return load4(B, row * D + col);
+}
+
+// Four elements at (row, col..col+3), columns clamped into the row. Values
+// for clamped columns are garbage; they only reach encoded columns >= D,
+// which are zeroed before Stage II.
+template <typename T>
+__device__ __forceinline__ float4 load_b4_any(const T* __restrict__ B, int64_t row, int64_t col,
+                                              int64_t D) {
   float v[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) v[q] = (col + q < D) ? load_elem(B, row * D + col + q) : 0.0f;
+  for (int q = 0; q < 4; ++q) v[q] = load_elem(B, row * D + (col + q < D ? col + q : D - 1));
   return make_float4(v[0], v[1], v[2], v[3]);
 }
 
+// Copy the first n floats of X into LDS: 16-byte loads and stores, all of a
+// thread's loads in flight at once. X is 16-byte aligned (base of a tensor).
+__device__ void copy_flat_to_lds(const float* __restrict__ X, float* xs, int n) {
+  const int tid = threadIdx.x;
+  const int n4 = n / 4;
+  const float4* src = reinterpret_cast<const float4*>(X);
+  float4* dst = reinterpret_cast<float4*>(xs);
+  constexpr int kBatch = 24;
+  for (int base = 0; base < n4; base += kThreads * kBatch) {
+    float4 v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = base + j * kThreads + tid;
+      v[j] = src[i < n4 ? i : 0];
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = base + j * kThreads + tid;
+      if (i < n4) dst[i] = v[j];
+    }
+  }
+  for (int i = 4 * n4 + tid; i < n; i += kThreads) xs[i] = X[i];
+}
+
+// Generic staging of an f-chunk [fc0, fc0+fcn) of rows [n0, n0+NB) (zero past
+// N) into xs[n*Pf + f - fc0].
+template <typename T>
+__device__ void stage_rows_chunk(const T* __restrict__ X, float* xs, int Pf, int n0, int NB, int F,
+                                 int N, int fc0, int fcn) {
+  for (int i = threadIdx.x; i < NB * fcn; i += kThreads) {
+    const int n = i / fcn, f = i - n * fcn;
+    xs[n * Pf + f] = (n0 + n < N) ? load_elem(X, (int64_t)(n0 + n) * F + fc0 + f) : 0.0f;
+  }
+}
+
+// The 16 C values C[k][d0..d0+15] of (sample, class) pair p = threadIdx.x,
+// loaded unconditionally with clamped addresses so the load count per thread
+// is fixed. No select is applied to the loaded values (that would force a
+// wait right here): pairs past N*K are never used and columns past D meet
+// zeroed encoded values.
+template <typename T>
+__device__ __forceinline__ void load_c_pair(const T* __restrict__ C, int K, int64_t D, int64_t d0,
+                                            int npairs, float (&c)[kW]) {
+  const int p = threadIdx.x;
+  const int k = p < npairs ? p % K : 0;
+  const T* crow = C + (int64_t)k * D;
+  if ((D & 15) == 0) {
+    // the block is 16 whole, aligned elements of the row: 4-element loads
+#pragma unroll
+    for (int j = 0; j < kW; j += 4) {
+      const float4 v = load4(crow, d0 + j);
+      c[j] = v.x;
+      c[j + 1] = v.y;
+      c[j + 2] = v.z;
+      c[j + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kW; ++j) c[j] = load_elem(crow, d0 + j < D ? d0 + j : D - 1);
+  }
+}
+
+// Partial similarity of one finished block: sl[n*K + k] += sum_c hs[n][c] C[k][d0+c]
+// (Eq. 8 restricted to the block's columns). hs is [NB][kW+1]; pair
+// threadIdx.x uses the preloaded cpair, further pairs read C directly.
+template <typename T>
+__device__ void block_scores(const T* __restrict__ C, const float* hs, float* sl, int npairs, int K,
+                             int64_t D, int64_t d0, const float (&cpair)[kW]) {
+  const int tid = threadIdx.x;
+  if (tid < npairs) {
+    const int n = tid / K;
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kW; ++j) s = fmaf(hs[n * (kW + 1) + j], cpair[j], s);
+    sl[tid] += s;
+  }
+  for (int p = tid + kThreads; p < npairs; p += kThreads) {
+    const int n = p / K, k = p - n * K;
+    const T* crow = C + (int64_t)k * D;
+    float s = 0.0f;
+    for (int j = 0; j < kW && d0 + j < D; ++j) s = fmaf(hs[n * (kW + 1) + j], load_elem(crow, d0 + j), s);
+    sl[p] += s;
+  }
+}
+
+// Publish this workgroup's partial scores (samples [nb0, nb0+nb)); after the
+// last sample block, take a ticket and, in the last workgroup, finish: sum
+// the replicas, write scores and labels, and re-zero the ticket.
+__device__ void publish_and_finish(const float* sl, int nb0, int nb, int N, int K, int R,
+                                   const SmallWs& ws, int32_t* __restrict__ labels,
+                                   float* __restrict__ scores, float* buf, int buf_floats,
+                                   bool finish) {
+  const int tid = threadIdx.x;
+  float* my = ws.sacc + (int64_t)(blockIdx.x % R) * N * K;
+  for (int p = tid; p < nb * K; p += kThreads) publish_add(my + (int64_t)nb0 * K + p, sl[p]);
+  if (!finish) return;
+  __shared__ int s_last;
+  wait_own_memory_ops();
+  __syncthreads();
+  if (tid == 0) s_last = (take_ticket(ws.counter) == gridDim.x - 1) ? 1 : 0;
+  __syncthreads();
+  if (!s_last) return;
+  const int64_t NK = (int64_t)N * K;
+  const int64_t total = (int64_t)R * NK;
+  if (total <= buf_floats) {
+    constexpr int kBatch = 16;
+    for (int64_t base = 0; base < total; base += (int64_t)kThreads * kBatch) {
+      float v[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int64_t i = base + (int64_t)j * kThreads + tid;
+        v[j] = i < total ? take_and_clear(ws.sacc + i) : 0.0f;
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int64_t i = base + (int64_t)j * kThreads + tid;
+        if (i < total) buf[i] = v[j];
+      }
+    }
+    __syncthreads();
+    for (int64_t o = tid; o < NK; o += kThreads) {
+      float s = 0.0f;
+      for (int r = 0; r < R; ++r) s += buf[r * NK + o];
+      buf[o] = s;  // replica 0's slot now holds the total
+      if (scores) scores[o] = s;
+    }
+    __syncthreads();
+    for (int n = tid; n < N; n += kThreads) {
+      float best = buf[(int64_t)n * K];
+      int best_k = 0;
+      for (int k = 1; k < K; ++k) {
+        const float s = buf[(int64_t)n * K + k];
+        if (s > best) {
+          best = s;
+          best_k = k;
+        }
+      }
+      labels[n] = best_k;
+    }
+  } else {
+    const int lane = tid & 63, wave = tid >> 6;
+    for (int n = wave; n < N; n += kWaves) {
+      float best = -__builtin_huge_valf();
+      int best_k = 0x7fffffff;
+      for (int k = lane; k < K; k += kWave) {
+        float t[kSmallReplicas];
+#pragma unroll
+        for (int r = 0; r < kSmallReplicas; ++r)
+          t[r] = r < R ? take_and_clear(ws.sacc + r * NK + (int64_t)n * K + k) : 0.0f;
+        float s = 0.0f;
+#pragma unroll
+        for (int r = 0; r < kSmallReplicas; ++r) s += t[r];
+        if (scores) scores[(int64_t)n * K + k] = s;
+        if (k == lane || s > best) {
+          best = s;
+          best_k = k;
+        }
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const float ob = __shfl_xor(best, off, kWave);
+        const int ok = __shfl_xor(best_k, off, kWave);
+        if (ob > best || (ob == best && ok < best_k)) {
+          best = ob;
+          best_k = ok;
+        }
+      }
+      if (lane == 0) labels[n] = best_k;
+    }
+  }
+  if (tid == 0) reset_counter(ws.counter);
+}
+
+// Sum of v over lanes {l, l+4, l+8, l+12} of each 16-lane row (DPP row
+// rotations, no LDS traffic).
+__device__ __forceinline__ float row_sum4(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                              0x128, 0xf, 0xf, false));  // row_ror:8
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                              0x124, 0xf, 0xf, false));  // row_ror:4
+  return v;
+}
+
+// Three-deep prefetch ring over a workgroup's items: while item i is
+// processed, items i+1 and i+2 are in flight. Buffers are named (no register
+// copies, which would wait on the loads). ring3_start issues the first two
+// items; the caller can do independent work before ring3_run.
+template <class Buf, class LoadF>
+__device__ __forceinline__ void ring3_start(int nitems, Buf& b0, Buf& b1, LoadF&& load) {
+  if (nitems <= 0) return;
+  load(b0, 0);
+  load(b1, nitems > 1 ? 1 : 0);
+}
+
+template <class Buf, class LoadF, class ProcF>
+__device__ __forceinline__ void ring3_run(int nitems, Buf& b0, Buf& b1, Buf& b2, LoadF&& load,
+                                          ProcF&& process) {
+  auto cl = [&](int i) { return i < nitems ? i : nitems - 1; };
+  for (int it = 0; it < nitems; it += 3) {
+    load(b2, cl(it + 2));
+    __builtin_amdgcn_sched_barrier(0);
+    process(b0, it);
+    if (it + 1 >= nitems) break;
+    load(b0, cl(it + 3));
+    __builtin_amdgcn_sched_barrier(0);
+    process(b1, it + 1);
+    if (it + 2 >= nitems) break;
+    load(b1, cl(it + 4));
+    __builtin_amdgcn_sched_barrier(0);
+    process(b2, it + 2);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// VALU kernel: NB samples per pass; 4 float4 column groups x 64 row groups.
+// Thread (cg, rg) handles columns 4cg..4cg+3 of a block and rows rg + 64u.
+// The thread's X values (rows rg + 64u of its NB samples) are the same for
+// every block; when F fits one chunk they are loaded once into registers.
+// LDS: xs[NB][FC] (only when F needs several chunks) | red[4][4][NB][16] |
+//      hs[NB][17] | sl[NB*K]
+// ---------------------------------------------------------------------------
+template <typename T, int NB>
+struct ValuBuf {
+  float4 b[kRpt];
+  float c[kW];
+};
+
 template <typename T, int NB, bool VEC>
-__global__ __launch_bounds__(kThreads) void small_fused_kernel(
+__global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
     const T* __restrict__ X, const T* __restrict__ B, const T* __restrict__ C,
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
-    int FC, void* __restrict__ workspace) {
-  constexpr int P = xs_pitch<NB>();
-  extern __shared__ float smem[];
-  float* xs = smem;                              // [FC][P]   X^T chunk
-  float* red = xs + FC * P;                      // [4][NB][32] per-wave column sums
-  float* hs = red + 4 * NB * kSmallCols;         // [NB][33]  encoded block
-  __shared__ int s_last;
-
+    int FC, int nblocks, int lds_floats, void* __restrict__ workspace) {
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  const int nchunks = (F + FC - 1) / FC;
+  const bool xcached = nchunks == 1;
+  float* xs = smem;
+  float* red = xs + (xcached ? 0 : NB * FC);  // [wave][row][NB][16]
+  float* hs = red + kWaves * 4 * NB * kW;
+  float* sl = hs + NB * (kW + 1);
   const SmallWs ws = small_ws(workspace);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int cg = tid % kColGroups, rg = tid / kColGroups;
-  const int g = blockIdx.x;
-  const int64_t d0 = (int64_t)g * kSmallCols;
-  const int64_t dcol = d0 + cg * 4;
-  const int R = gridDim.x < kSmallReplicas ? (int)gridDim.x : kSmallReplicas;
-  float* my_sacc = ws.sacc + (int64_t)(g % R) * N * K;
+  const int cg = tid % kCG, rg = tid / kCG;
+  const int G = gridDim.x;
+  const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
+  const int R = replicas(G);
+  const int nmine = walk.count();
+  const int nitems = nmine * nchunks;
 
   for (int nb0 = 0; nb0 < N; nb0 += NB) {
-    float acc[NB][4];
-#pragma unroll
-    for (int n = 0; n < NB; ++n) acc[n][0] = acc[n][1] = acc[n][2] = acc[n][3] = 0.0f;
+    const int nb = min(NB, N - nb0);
+    const int npairs = nb * K;
+    for (int p = tid; p < NB * K; p += kThreads) sl[p] = 0.0f;
 
-    for (int fc0 = 0; fc0 < F; fc0 += FC) {
-      const int fcn = min(FC, F - fc0);
-      const int jmax = (fcn + kRowGroups - 1) / kRowGroups;  // row batches are uniform
-      float4 b0[kRowsPerBatch], b1[kRowsPerBatch];
-      auto load_batch = [&](float4(&dst)[kRowsPerBatch], int j0) {
+    // Items are (block, chunk) pairs in this workgroup's order.
+    auto load = [&](ValuBuf<T, NB>& x, int it) {
+      const int blk = walk.block_of(it / nchunks), ch = it % nchunks;
+      const int64_t col = (int64_t)blk * kW + cg * 4;
+      const int f0 = ch * FC, fcn = min(FC, F - f0);
 #pragma unroll
-        for (int u = 0; u < kRowsPerBatch; ++u) {
-          const int f = rg + kRowGroups * (j0 + u);
-          dst[u] = (f < fcn) ? load_b4<T, VEC>(B, fc0 + f, dcol, D) : make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int u = 0; u < kRpt; ++u) {
+        // rows past the chunk are clamped (their X factor is zero or the row
+        // is skipped); columns past D give garbage zeroed after encoding
+        const int f = rg + kRG * u;
+        const int fc = f < fcn ? f : fcn - 1;
+        x.b[u] = VEC ? load_b4_vec(B, f0 + fc, col < D ? col : 0, D)
+                     : load_b4_any(B, f0 + fc, col, D);
+      }
+      load_c_pair(C, K, D, (int64_t)blk * kW, npairs, x.c);
+    };
+
+    ValuBuf<T, NB> b0, b1, b2;
+    ring3_start(nitems, b0, b1, load);  // B is in flight while X is fetched
+    float xr[kRpt][NB];
+    if (xcached) {
+#pragma unroll
+      for (int u = 0; u < kRpt; ++u) {
+        const int f = rg + kRG * u;
+#pragma unroll
+        for (int n = 0; n < NB; ++n) {
+          const float v = load_elem(X, (int64_t)(nb0 + (n < nb ? n : 0)) * F + (f < F ? f : 0));
+          xr[u][n] = (f < F && n < nb) ? v : 0.0f;
         }
-      };
-      auto compute_batch = [&](const float4(&src)[kRowsPerBatch], int j0) {
+      }
+    }
+
+    float acc[NB][4];
+    auto process = [&](const ValuBuf<T, NB>& x, int it) {
+      const int blk = walk.block_of(it / nchunks), ch = it % nchunks;
+      const int f0 = ch * FC, fcn = min(FC, F - f0);
+      const int64_t d0 = (int64_t)blk * kW;
+      if (ch == 0) {
 #pragma unroll
-        for (int u = 0; u < kRowsPerBatch; ++u) {
-          const int f = rg + kRowGroups * (j0 + u);
+        for (int n = 0; n < NB; ++n) acc[n][0] = acc[n][1] = acc[n][2] = acc[n][3] = 0.0f;
+      }
+      if (xcached) {
+#pragma unroll
+        for (int u = 0; u < kRpt; ++u)
+#pragma unroll
+          for (int n = 0; n < NB; ++n) {
+            const float xv = xr[u][n];
+            acc[n][0] = fmaf(xv, x.b[u].x, acc[n][0]);
+            acc[n][1] = fmaf(xv, x.b[u].y, acc[n][1]);
+            acc[n][2] = fmaf(xv, x.b[u].z, acc[n][2]);
+            acc[n][3] = fmaf(xv, x.b[u].w, acc[n][3]);
+          }
+      } else {
+        __syncthreads();
+        stage_rows_chunk(X, xs, FC, nb0, NB, F, N, f0, fcn);
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kRpt; ++u) {
+          const int f = rg + kRG * u;
           if (f < fcn) {
-            const float* xrow = xs + f * P;
 #pragma unroll
             for (int n = 0; n < NB; ++n) {
-              const float x = xrow[n];
-              acc[n][0] = fmaf(x, src[u].x, acc[n][0]);
-              acc[n][1] = fmaf(x, src[u].y, acc[n][1]);
-              acc[n][2] = fmaf(x, src[u].z, acc[n][2]);
-              acc[n][3] = fmaf(x, src[u].w, acc[n][3]);
+              const float xv = xs[n * FC + f];
+              acc[n][0] = fmaf(xv, x.b[u].x, acc[n][0]);
+              acc[n][1] = fmaf(xv, x.b[u].y, acc[n][1]);
+              acc[n][2] = fmaf(xv, x.b[u].z, acc[n][2]);
+              acc[n][3] = fmaf(xv, x.b[u].w, acc[n][3]);
             }
           }
         }
-      };
-
-      // Issue the first B batch before staging X so both latencies overlap.
-      load_batch(b0, 0);
-      __syncthreads();  // previous readers of xs are done
-      for (int i = tid; i < NB * fcn; i += kThreads) {
-        const int n = i / fcn, f = i - n * fcn;
-        xs[f * P + n] = (nb0 + n < N) ? load_elem(X, (int64_t)(nb0 + n) * F + fc0 + f) : 0.0f;
       }
-      __syncthreads();
-      for (int j0 = 0; j0 < jmax; j0 += 2 * kRowsPerBatch) {
-        const bool more1 = j0 + kRowsPerBatch < jmax;
-        if (more1) load_batch(b1, j0 + kRowsPerBatch);
-        compute_batch(b0, j0);
-        if (more1) {
-          if (j0 + 2 * kRowsPerBatch < jmax) load_batch(b0, j0 + 2 * kRowsPerBatch);
-          compute_batch(b1, j0 + kRowsPerBatch);
-        }
-      }
-    }
-
-    // Sum the 8 row groups of this wave (lanes differing in bits 3..5).
-#pragma unroll
-    for (int n = 0; n < NB; ++n)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float v = acc[n][q];
-        v += __shfl_xor(v, 8, kWave);
-        v += __shfl_xor(v, 16, kWave);
-        v += __shfl_xor(v, 32, kWave);
-        acc[n][q] = v;
-      }
-    if (lane < kColGroups) {
+      if (ch != nchunks - 1) return;
+      // Lane l of a wave is (cg = l%4, row group = l/4). DPP sums the 4 row
+      // groups of each 16-lane row; lanes 0..3 of each row then hold the
+      // row's partial for their columns.
+      __syncthreads();  // previous block's readers of red / hs are done
 #pragma unroll
       for (int n = 0; n < NB; ++n)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) red[(wave * NB + n) * kSmallCols + lane * 4 + q] = acc[n][q];
-    }
-    __syncthreads();
-    for (int i = tid; i < NB * kSmallCols; i += kThreads) {
-      const int n = i / kSmallCols, c = i % kSmallCols;
-      const float v = (red[(0 * NB + n) * kSmallCols + c] + red[(1 * NB + n) * kSmallCols + c]) +
-                      (red[(2 * NB + n) * kSmallCols + c] + red[(3 * NB + n) * kSmallCols + c]);
-      const bool valid = (d0 + c < D) && (nb0 + n < N);
-      hs[n * 33 + c] = valid ? activate(v, act) : 0.0f;
-    }
-    __syncthreads();
-    // Partial similarity of this column block (Eq. 8 restricted to 32 dims).
-    const int ncols = (int)min((int64_t)kSmallCols, (int64_t)D - d0);
-    for (int p = tid; p < NB * K; p += kThreads) {
-      const int n = p / K, k = p - n * K;
-      if (nb0 + n >= N) continue;
-      const T* crow = C + (int64_t)k * D + d0;
-      const float* hrow = hs + n * 33;
-      float s = 0.0f;
-      for (int c = 0; c < ncols; ++c) s = fmaf(hrow[c], load_elem(crow, c), s);
-      unsafeAtomicAdd(my_sacc + (int64_t)(nb0 + n) * K + k, s);
-    }
-  }
-
-  // Ticket: the last workgroup to arrive finishes the reduction.
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = (atomicAdd(ws.counter, 1u) == gridDim.x - 1) ? 1 : 0;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-
-  const int64_t NK = (int64_t)N * K;
-  for (int n = wave; n < N; n += kThreads / kWave) {
-    float best = -__builtin_huge_valf();
-    int best_k = 0x7fffffff;
-    for (int k = lane; k < K; k += kWave) {
-      float s = 0.0f;
-      for (int r = 0; r < R; ++r) s += load_coherent(ws.sacc + r * NK + (int64_t)n * K + k);
-      if (scores) scores[(int64_t)n * K + k] = s;
-      if (k == lane || s > best) {
-        best = s;
-        best_k = k;
-      }
-    }
+        for (int q = 0; q < 4; ++q) {
+          const float v = row_sum4(acc[n][q]);
+          if ((lane & 15) < kCG)
+            red[((wave * 4 + (lane >> 4)) * NB + n) * kW + (lane & 3) * 4 + q] = v;
+        }
+      __syncthreads();
+      for (int i = tid; i < NB * kW; i += kThreads) {
+        const int n = i / kW, c = i % kW;
+        float v = 0.0f;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const float ob = __shfl_xor(best, off, kWave);
-      const int ok = __shfl_xor(best_k, off, kWave);
-      if (ob > best || (ob == best && ok < best_k)) {
-        best = ob;
-        best_k = ok;
+        for (int w = 0; w < kWaves * 4; ++w) v += red[(w * NB + n) * kW + c];
+        hs[n * (kW + 1) + c] = (d0 + c < D && n < nb) ? activate(v, act) : 0.0f;
       }
-    }
-    if (lane == 0) labels[n] = best_k;
+      __syncthreads();
+      block_scores(C, hs, sl, npairs, K, D, d0, x.c);
+    };
+
+    ring3_run(nitems, b0, b1, b2, load, process);
+    __syncthreads();
+    publish_and_finish(sl, nb0, nb, N, K, R, ws, labels, scores, smem, lds_floats,
+                       nb0 + NB >= N);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Matrix-core kernel (fp32, 8 < N <= 64): NTI sample tiles of 16, MS 4-row
+// steps per wave. Wave w accumulates V^T[16 d x 16 n] per sample tile over
+// its quarter of the F rows; the waves' partials are summed through LDS.
+//   A operand (16x16x4 f32): lane l holds B[f0 + l/16][d0 + l%16]
+//   B operand: lane l holds X[16t + l%16][f0 + l/16]; these values do not
+//     depend on the column block, so each wave loads them once into registers
+//   result: lane l, reg r holds V^T[d0 + 4(l/16) + r][16t + l%16]
+// LDS: red[4][NTI][16][16] | hs[16*NTI][17] | sl[16*NTI*K]
+// ---------------------------------------------------------------------------
+template <int MS>
+struct MfmaBuf {
+  float a[MS];
+  float c[kW];
+};
+
+template <int NTI, int MS>
+__global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
+    const float* __restrict__ X, const float* __restrict__ B, const float* __restrict__ C,
+    int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
+    int nblocks, int lds_floats, void* __restrict__ workspace) {
+  constexpr int NB = 16 * NTI;
+  constexpr int FQ = 4 * MS;                  // rows per wave
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  float* sl = smem;                                // [NB*K]
+  float* red = sl + (NB * K + 3) / 4 * 4;          // [4][NTI][256]
+  float* hs = red + kWaves * NTI * 256;            // [NB][17]
+  float* xs = red;  // [nb][F]: X rows, only until the operands are in registers
+  const SmallWs ws = small_ws(workspace);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int G = gridDim.x;
+  const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
+  const int R = replicas(G);
+  const int nb = min(NB, N);
+  const int npairs = nb * K;
+  const int arow = wave * FQ + (lane >> 4);  // A-operand row of step 0
+  const int acol = lane & 15;
+  const int nmine = walk.count();
+
+  auto load = [&](MfmaBuf<MS>& x, int i) {
+    const int64_t col = (int64_t)walk.block_of(i) * kW + acol;
+    const int64_t cc = col < D ? col : D - 1;
+#pragma unroll
+    for (int s = 0; s < MS; ++s) {
+      // rows past F are clamped and meet zero X values; columns past D give
+      // garbage that is zeroed after encoding
+      const int f = arow + 4 * s;
+      x.a[s] = B[(int64_t)(f < F ? f : F - 1) * D + cc];
+    }
+    load_c_pair(C, K, D, (int64_t)walk.block_of(i) * kW, npairs, x.c);
+  };
+
+  // B is in flight while X (rows 0..nb-1, one contiguous range) is copied to
+  // LDS and each wave's operand values are read back into registers.
+  MfmaBuf<MS> b0, b1, b2;
+  ring3_start(nmine, b0, b1, load);
+  for (int p = tid; p < NB * K; p += kThreads) sl[p] = 0.0f;
+  copy_flat_to_lds(X, xs, nb * F);
   __syncthreads();
-  for (int64_t i = tid; i < (int64_t)R * NK; i += kThreads) store_coherent(ws.sacc + i, 0.0f);
-  if (tid == 0) __hip_atomic_store(ws.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  float xr[MS][NTI];
+#pragma unroll
+  for (int s = 0; s < MS; ++s)
+#pragma unroll
+    for (int t = 0; t < NTI; ++t) {
+      const int n = 16 * t + (lane & 15), f = arow + 4 * s;
+      const float v = xs[(n < nb ? n : 0) * F + (f < F ? f : 0)];
+      xr[s][t] = (n < nb && f < F) ? v : 0.0f;
+    }
+
+  auto process = [&](const MfmaBuf<MS>& x, int i) {
+    const int64_t d0 = (int64_t)walk.block_of(i) * kW;
+    f32x4 acc[NTI];
+#pragma unroll
+    for (int t = 0; t < NTI; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < MS; ++s)
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[s], xr[s][t], acc[t], 0, 0, 0);
+    __syncthreads();  // previous block's readers of red / hs are done
+#pragma unroll
+    for (int t = 0; t < NTI; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        red[(wave * NTI + t) * 256 + (4 * (lane >> 4) + r) * 16 + (lane & 15)] = acc[t][r];
+    __syncthreads();
+    for (int e = tid; e < NB * kW; e += kThreads) {
+      const int n = e / kW, c = e % kW;
+      const int t = n / 16, j = n % 16;
+      float v = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) v += red[(w * NTI + t) * 256 + c * 16 + j];
+      hs[n * (kW + 1) + c] = (d0 + c < D && n < nb) ? activate(v, act) : 0.0f;
+    }
+    __syncthreads();
+    block_scores(C, hs, sl, npairs, K, D, d0, x.c);
+  };
+
+  ring3_run(nmine, b0, b1, b2, load, process);
+  __syncthreads();
+  publish_and_finish(sl, 0, nb, N, K, R, ws, labels, scores, smem, lds_floats, true);
+}
+
+int num_cus() {
+  static const int cus = [] {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        v <= 0)
+      return 256;
+    return v;
+  }();
+  return cus;
+}
+
+constexpr int kMfmaSteps[] = {12, 24, 36, 48};  // 4-row steps per wave: F <= 16 * MS
+
+struct SmallPlan {
+  bool mfma;
+  int nb;    // VALU samples per pass, or MFMA sample tiles
+  int ms;    // MFMA steps per wave
+  int FC;    // VALU f-chunk
+  size_t lds;
+  int grid;
+  int nblocks;
+};
+
+SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  SmallPlan p{};
+  p.nblocks = (int)cdiv(D, kW);
+  p.grid = p.nblocks < num_cus() ? p.nblocks : num_cus();
+  const int nti = (int)cdiv(N, 16);
+  if (dt == 0 && N > 8) {
+    for (int ms : kMfmaSteps) {
+      if ((int64_t)16 * ms < F) continue;
+      const int64_t scratch = kWaves * nti * 256 + 16 * nti * (kW + 1);
+      const int64_t lds = (int64_t)sizeof(float) *
+                          ((16 * nti * K + 3) / 4 * 4 + (scratch > N * F ? scratch : N * F));
+      if (lds <= kLdsBudget) {
+        p.mfma = true;
+        p.nb = nti;
+        p.ms = ms;
+        p.lds = (size_t)lds;
+        return p;
+      }
+      break;
+    }
+  }
+  const int nb = N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : N <= 8 ? 8 : N <= 16 ? 16 : 32;
+  const int64_t fixed =
+      (int64_t)sizeof(float) * (kWaves * 4 * nb * kW + nb * (kW + 1) + nb * K);
+  if (fixed > kLdsBudget) return p;  // nb * K too large for LDS: unsupported
+  if (F <= kRG * kRpt) {
+    p.FC = (int)F;  // one chunk: X lives in registers, no staging area
+    p.lds = (size_t)fixed;
+  } else {
+    int64_t fc = (kLdsBudget - fixed) / (int64_t)(sizeof(float) * nb);
+    if (fc > kRG * kRpt) fc = kRG * kRpt;  // one chunk holds at most kRG*kRpt rows
+    if (fc < 1) return p;
+    p.FC = (int)fc;
+    p.lds = (size_t)fixed + sizeof(float) * (size_t)fc * nb;
+  }
+  p.nb = nb;
+  return p;
+}
+
+// The last workgroup reuses all of LDS to sum the R score replicas, so give
+// the launch at least R*N*K floats when that fits.
+void widen_for_final(SmallPlan& p, int64_t N, int64_t K) {
+  const size_t want = sizeof(float) * (size_t)replicas(p.grid) * N * K;
+  if (p.lds < want && want <= (size_t)kLdsBudget) p.lds = want;
+}
+
+template <typename KernelT>
+hipError_t allow_lds(KernelT* k) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget);
 }
 
 template <typename T, int NB, bool VEC>
-hipError_t launch_nb(const void* X, const void* B, const void* C, int32_t* labels, float* scores,
-                     int N, int F, int D, int K, int act, void* ws, hipStream_t stream) {
-  constexpr int P = xs_pitch<NB>();
-  int FC = kXsFloats / P;
-  if (FC > F) FC = F;
-  const size_t lds = sizeof(float) * ((size_t)FC * P + 4 * NB * kSmallCols + NB * 33);
-  const int G = (int)cdiv(D, kSmallCols);
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&small_fused_kernel<T, NB, VEC>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024);
+hipError_t launch_valu(const SmallPlan& p, const void* X, const void* B, const void* C,
+                       int32_t* labels, float* scores, int N, int F, int D, int K, int act,
+                       void* ws, hipStream_t stream) {
+  static const hipError_t attr = allow_lds(&small_valu_kernel<T, NB, VEC>);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((small_fused_kernel<T, NB, VEC>), dim3(G), dim3(kThreads), lds, stream,
-                     (const T*)X, (const T*)B, (const T*)C, labels, scores, N, F, D, K, act, FC,
-                     ws);
+  hipLaunchKernelGGL((small_valu_kernel<T, NB, VEC>), dim3(p.grid), dim3(kThreads), p.lds, stream,
+                     (const T*)X, (const T*)B, (const T*)C, labels, scores, N, F, D, K, act, p.FC,
+                     p.nblocks, (int)(p.lds / sizeof(float)), ws);
   return hipGetLastError();
 }
 
+template <int NTI, int MS>
+hipError_t launch_mfma(const SmallPlan& p, const void* X, const void* B, const void* C,
+                       int32_t* labels, float* scores, int N, int F, int D, int K, int act,
+                       void* ws, hipStream_t stream) {
+  static const hipError_t attr = allow_lds(&small_mfma_kernel<NTI, MS>);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((small_mfma_kernel<NTI, MS>), dim3(p.grid), dim3(kThreads), p.lds, stream,
+                     (const float*)X, (const float*)B, (const float*)C, labels, scores, N, F, D, K,
+                     act, p.nblocks, (int)(p.lds / sizeof(float)), ws);
+  return hipGetLastError();
+}
+
+template <int NTI>
+hipError_t launch_mfma_ms(const SmallPlan& p, const void* X, const void* B, const void* C,
+                          int32_t* labels, float* scores, int N, int F, int D, int K, int act,
+                          void* ws, hipStream_t stream) {
+  switch (p.ms) {
+    case 12: return launch_mfma<NTI, 12>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 24: return launch_mfma<NTI, 24>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 36: return launch_mfma<NTI, 36>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    default: return launch_mfma<NTI, 48>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+  }
+}
+
 template <typename T, bool VEC>
-hipError_t launch_t(const void* X, const void* B, const void* C, int32_t* labels, float* scores,
-                    int N, int F, int D, int K, int act, void* ws, hipStream_t stream) {
-  if (N <= 1) return launch_nb<T, 1, VEC>(X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-  if (N <= 2) return launch_nb<T, 2, VEC>(X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-  if (N <= 4) return launch_nb<T, 4, VEC>(X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-  if (N <= 8) return launch_nb<T, 8, VEC>(X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-  if (N <= 16) return launch_nb<T, 16, VEC>(X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-  return launch_nb<T, 32, VEC>(X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+hipError_t launch_valu_t(const SmallPlan& p, const void* X, const void* B, const void* C,
+                         int32_t* labels, float* scores, int N, int F, int D, int K, int act,
+                         void* ws, hipStream_t stream) {
+  switch (p.nb) {
+    case 1: return launch_valu<T, 1, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 2: return launch_valu<T, 2, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 4: return launch_valu<T, 4, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 8: return launch_valu<T, 8, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 16: return launch_valu<T, 16, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    default: return launch_valu<T, 32, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+  }
 }
 
 }  // namespace
 
-size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K) {
-  (void)F;
-  const int64_t G = cdiv(D, kSmallCols);
-  const int64_t R = G < kSmallReplicas ? G : kSmallReplicas;
-  return 256 + sizeof(float) * (size_t)(R * N * K);
+bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  return plan_small(N, F, D, K, dt).nb > 0;
+}
+
+size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  const SmallPlan p = plan_small(N, F, D, K, dt);
+  return 256 + sizeof(float) * (size_t)replicas(p.grid) * N * K;
 }
 
 hipError_t launch_small(const void* X, const void* B, const void* C, int32_t* labels,
                         float* scores, int64_t N, int64_t F, int64_t D, int64_t K, int dt,
                         int act, void* workspace, hipStream_t stream) {
+  SmallPlan p = plan_small(N, F, D, K, dt);
+  widen_for_final(p, N, K);
+  if (p.nb == 0) return hipErrorInvalidValue;
+  const int n = (int)N, f = (int)F, d = (int)D, k = (int)K;
+  if (p.mfma) {
+    switch (p.nb) {
+      case 1: return launch_mfma_ms<1>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+      case 2: return launch_mfma_ms<2>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+      case 3: return launch_mfma_ms<3>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+      default: return launch_mfma_ms<4>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+    }
+  }
   const size_t align = dt == 0 ? 16 : 8;
   const bool vec = (D % 4 == 0) && ((uintptr_t)B % align == 0);
-  const int n = (int)N, f = (int)F, d = (int)D, k = (int)K;
   if (dt == 0)
-    return vec ? launch_t<float, true>(X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
-               : launch_t<float, false>(X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
-  return vec ? launch_t<bf16raw, true>(X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
-             : launch_t<bf16raw, false>(X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+    return vec ? launch_valu_t<float, true>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
+               : launch_valu_t<float, false>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+  return vec ? launch_valu_t<bf16raw, true>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
+             : launch_valu_t<bf16raw, false>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
 }
 
 }  // namespace hd

@@ -180,7 +180,13 @@ def test_packed_model_matches_raw(hd, N, dtype):
     y0, S0 = run(hd, X, B, C, dtype)
     y1, S1 = run(hd, X, B, C, dtype, packed=True)
     assert np.array_equal(y0, y1)
-    assert np.array_equal(S0, S1)
+    if N > 64:
+        assert np.array_equal(S0, S1)  # the large-batch path is deterministic
+    else:
+        # the small-batch path sums partial scores with fp32 atomics, so the
+        # order (and the last bits) can change between calls
+        c1 = np.abs(C.astype(np.float64)).sum(axis=1)
+        assert np.all(np.abs(S0 - S1) <= 1e-6 * c1[None, :])
 
 
 # --- the stages alone -----------------------------------------------------------
