@@ -564,6 +564,111 @@ __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
   publish_and_finish(sl, 0, nb, N, K, R, ws, labels, scores, smem, lds_floats, true);
 }
 
+// ---------------------------------------------------------------------------
+// Flat kernel (N <= 8, one column block per workgroup). Every load a
+// workgroup needs (its block of B, its rows of X, its pairs' C values) is
+// issued at entry; several workgroups share a CU, so the hardware overlaps
+// them. Thread (cg, rg) handles columns 4cg..4cg+3 and rows rg + 64u of
+// each f-chunk of 64*RPT rows.
+// LDS: red[16][NB][16] | hs[NB][17]
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int xcd_block(int b, int G) {
+  // contiguous column ranges per XCD (blocks sharing L2 lines meet in one L2)
+  const int per = G / 8, rem = G % 8, x = b % 8, j = b / 8;
+  return x * per + min(x, rem) + j;
+}
+
+template <typename T, int NB, int RPT, bool VEC>
+__global__ __launch_bounds__(kThreads) void small_flat_kernel(
+    const T* __restrict__ X, const T* __restrict__ B, const T* __restrict__ C,
+    int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
+    void* __restrict__ workspace) {
+  constexpr int kChunk = kRG * RPT;
+  __shared__ float red[kWaves * 4 * NB * kW];
+  __shared__ float hs[NB * (kW + 1)];
+  const SmallWs ws = small_ws(workspace);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cg = tid % kCG, rg = tid / kCG;
+  const int G = gridDim.x;
+  const int blk = xcd_block(blockIdx.x, G);
+  const int R = replicas(G);
+  const int64_t d0 = (int64_t)blk * kW;
+  const int64_t col = d0 + cg * 4;
+  const int64_t colc = col < D ? col : 0;
+  const int npairs = N * K;
+
+  float cpair[kW];
+  load_c_pair(C, K, D, d0, npairs, cpair);
+  float acc[NB][4];
+#pragma unroll
+  for (int n = 0; n < NB; ++n) acc[n][0] = acc[n][1] = acc[n][2] = acc[n][3] = 0.0f;
+  for (int f0 = 0; f0 < F; f0 += kChunk) {
+    float4 b[RPT];
+    float x[RPT][NB];
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) {
+      // rows past F are clamped and get a zero X factor; columns past D
+      // give garbage that is zeroed after encoding
+      const int f = f0 + rg + kRG * u;
+      const int fc = f < F ? f : F - 1;
+      b[u] = VEC ? load_b4_vec(B, fc, colc, D) : load_b4_any(B, fc, col, D);
+    }
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) {
+      const int f = f0 + rg + kRG * u;
+#pragma unroll
+      for (int n = 0; n < NB; ++n) {
+        const float v = load_elem(X, (int64_t)(n < N ? n : 0) * F + (f < F ? f : 0));
+        x[u][n] = (f < F && n < N) ? v : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < RPT; ++u)
+#pragma unroll
+      for (int n = 0; n < NB; ++n) {
+        acc[n][0] = fmaf(x[u][n], b[u].x, acc[n][0]);
+        acc[n][1] = fmaf(x[u][n], b[u].y, acc[n][1]);
+        acc[n][2] = fmaf(x[u][n], b[u].z, acc[n][2]);
+        acc[n][3] = fmaf(x[u][n], b[u].w, acc[n][3]);
+      }
+  }
+  // lanes 16r..16r+15 hold 4 row groups x 4 column groups: DPP sums the row
+  // groups, then the 16 (wave, row) partials are summed through LDS
+#pragma unroll
+  for (int n = 0; n < NB; ++n)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float v = row_sum4(acc[n][q]);
+      if ((lane & 15) < kCG) red[((wave * 4 + (lane >> 4)) * NB + n) * kW + (lane & 3) * 4 + q] = v;
+    }
+  __syncthreads();
+  if (tid < NB * kW) {
+    const int n = tid / kW, c = tid % kW;
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves * 4; ++w) v += red[(w * NB + n) * kW + c];
+    hs[n * (kW + 1) + c] = (d0 + c < D && n < N) ? activate(v, act) : 0.0f;
+  }
+  __syncthreads();
+  float* my = ws.sacc + (int64_t)(blockIdx.x % R) * N * K;
+  if (tid < npairs) {
+    const int n = tid / K;
+    float sc = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kW; ++j) sc = fmaf(hs[n * (kW + 1) + j], cpair[j], sc);
+    publish_add(my + tid, sc);
+  }
+  for (int p = tid + kThreads; p < npairs; p += kThreads) {
+    const int n = p / K, k = p - n * K;
+    const T* crow = C + (int64_t)k * D;
+    float sc = 0.0f;
+    for (int j = 0; j < kW && d0 + j < D; ++j) sc = fmaf(hs[n * (kW + 1) + j], load_elem(crow, d0 + j), sc);
+    publish_add(my + p, sc);
+  }
+  float none[1] = {0.0f};
+  publish_and_finish(none, 0, 0, N, K, R, ws, labels, scores, red, kWaves * 4 * NB * kW, true);
+}
+
 int num_cus() {
   static const int cus = [] {
     int dev = 0, v = 0;
@@ -579,6 +684,8 @@ int num_cus() {
 constexpr int kMfmaSteps[] = {12, 24, 36, 48};  // 4-row steps per wave: F <= 16 * MS
 
 struct SmallPlan {
+  bool flat;  // one block per workgroup (N <= 8)
+  int rpt;    // flat kernel: rows per thread per chunk
   bool mfma;
   int nb;    // VALU samples per pass, or MFMA sample tiles
   int ms;    // MFMA steps per wave
@@ -591,6 +698,13 @@ struct SmallPlan {
 SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   SmallPlan p{};
   p.nblocks = (int)cdiv(D, kW);
+  if (N <= 8) {
+    p.flat = true;
+    p.nb = N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : 8;
+    p.rpt = F <= kRG * 4 ? 4 : F <= kRG * 6 ? 6 : F <= kRG * 9 ? 9 : F <= kRG * 12 ? 12 : 16;
+    p.grid = p.nblocks;
+    return p;
+  }
   p.grid = p.nblocks < num_cus() ? p.nblocks : num_cus();
   const int nti = (int)cdiv(N, 16);
   if (dt == 0 && N > 8) {
@@ -701,10 +815,54 @@ size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt)
   return 256 + sizeof(float) * (size_t)replicas(p.grid) * N * K;
 }
 
+template <typename T, int NB, int RPT, bool VEC>
+hipError_t launch_flat(const SmallPlan& p, const void* X, const void* B, const void* C,
+                       int32_t* labels, float* scores, int N, int F, int D, int K, int act,
+                       void* ws, hipStream_t stream) {
+  hipLaunchKernelGGL((small_flat_kernel<T, NB, RPT, VEC>), dim3(p.grid), dim3(kThreads), 0, stream,
+                     (const T*)X, (const T*)B, (const T*)C, labels, scores, N, F, D, K, act, ws);
+  return hipGetLastError();
+}
+
+template <typename T, int NB, bool VEC>
+hipError_t launch_flat_rpt(const SmallPlan& p, const void* X, const void* B, const void* C,
+                           int32_t* labels, float* scores, int N, int F, int D, int K, int act,
+                           void* ws, hipStream_t stream) {
+  switch (p.rpt) {
+    case 4: return launch_flat<T, NB, 4, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 6: return launch_flat<T, NB, 6, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 9: return launch_flat<T, NB, 9, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 12: return launch_flat<T, NB, 12, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    default: return launch_flat<T, NB, 16, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+  }
+}
+
+template <typename T, bool VEC>
+hipError_t launch_flat_t(const SmallPlan& p, const void* X, const void* B, const void* C,
+                         int32_t* labels, float* scores, int N, int F, int D, int K, int act,
+                         void* ws, hipStream_t stream) {
+  switch (p.nb) {
+    case 1: return launch_flat_rpt<T, 1, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 2: return launch_flat_rpt<T, 2, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 4: return launch_flat_rpt<T, 4, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    default: return launch_flat_rpt<T, 8, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+  }
+}
+
 hipError_t launch_small(const void* X, const void* B, const void* C, int32_t* labels,
                         float* scores, int64_t N, int64_t F, int64_t D, int64_t K, int dt,
                         int act, void* workspace, hipStream_t stream) {
   SmallPlan p = plan_small(N, F, D, K, dt);
+  if (p.flat) {
+    const size_t align = dt == 0 ? 16 : 8;
+    const bool vec = (D % 4 == 0) && ((uintptr_t)B % align == 0);
+    const int n = (int)N, f = (int)F, d = (int)D, k = (int)K;
+    if (dt == 0)
+      return vec ? launch_flat_t<float, true>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
+                 : launch_flat_t<float, false>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+    return vec ? launch_flat_t<bf16raw, true>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
+               : launch_flat_t<bf16raw, false>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+  }
   widen_for_final(p, N, K);
   if (p.nb == 0) return hipErrorInvalidValue;
   const int n = (int)N, f = (int)F, d = (int)D, k = (int)K;
