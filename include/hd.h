@@ -123,6 +123,14 @@ hd_status hd_infer_packed(const void *X, const void *packed, int32_t *labels, fl
                           int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,
                           void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Introspection: the name of the main kernel that hd_infer (packed == 0) or
+ * hd_infer_packed (packed != 0) launches for these sizes, assuming 16-byte
+ * aligned operands; "" when the call would be rejected. The returned string
+ * is static. Used by benchmarks and profilers to find the kernel's dispatches.
+ */
+const char *hd_infer_kernel(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, int packed);
+
 #ifdef __cplusplus
 }
 #endif

@@ -31,6 +31,7 @@ SYMBOLS = (
     "hd_pack_model",
     "hd_infer_packed_workspace_bytes",
     "hd_infer_packed",
+    "hd_infer_kernel",
 )
 
 _lib = None
@@ -76,6 +77,8 @@ def lib():
         L.hd_infer_packed_workspace_bytes.restype = sz
         L.hd_infer_packed.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, i32, vp, sz, vp]
         L.hd_infer_packed.restype = i32
+        L.hd_infer_kernel.argtypes = [i64, i64, i64, i64, i32, i32]
+        L.hd_infer_kernel.restype = ctypes.c_char_p
         _lib = L
         return L
 
@@ -170,6 +173,13 @@ def infer_workspace_bytes(N: int, F: int, D: int, K: int, dtype) -> int:
     torch = _torch()
     dt = HD_F32 if dtype == torch.float32 else HD_BF16
     return int(lib().hd_infer_workspace_bytes(N, F, D, K, dt))
+
+
+def infer_kernel(N: int, F: int, D: int, K: int, dtype, packed: bool = True) -> str:
+    """Name of the main kernel hd_infer / hd_infer_packed launches for these sizes."""
+    torch = _torch()
+    dt = HD_F32 if dtype == torch.float32 else HD_BF16
+    return lib().hd_infer_kernel(N, F, D, K, dt, 1 if packed else 0).decode()
 
 
 def infer(X, B, C, act: str = "hardsign", return_scores: bool = False, out=None,

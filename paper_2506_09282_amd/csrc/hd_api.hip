@@ -25,21 +25,24 @@ hd_status from_hip(hipError_t e) { return e == hipSuccess ? HD_OK : HD_ERR_HIP; 
 
 size_t esize(int dt) { return dt == HD_F32 ? 4 : 2; }
 
-// Packed model image: [tiled B and C for the matrix-core path | B as given |
-// C as given]. The natural-layout copies serve the small-batch path, which
-// streams B row segments directly.
+// Packed model image: [fragment-tiled B and C for the matrix-core path |
+// column-tiled B and C for the small-batch path]. Both sections start on a
+// 256-byte boundary of the (256-byte aligned) image.
 struct Image {
-  size_t tiled, raw_b, raw_c, total;
+  size_t large, small, total;
 };
 
 Image image_layout(int64_t F, int64_t D, int64_t K, int dt) {
   Image im;
-  im.tiled = align256(hd::large_packed_bytes(F, D, K, dt));
-  im.raw_b = align256((size_t)F * D * esize(dt));
-  im.raw_c = align256((size_t)K * D * esize(dt));
-  im.total = im.tiled + im.raw_b + im.raw_c;
+  im.large = align256(hd::large_packed_bytes(F, D, K, dt));
+  im.small = align256(hd::small_packed_bytes(F, D, K, dt));
+  im.total = im.large + im.small;
   return im;
 }
+
+// Every element pointer must be aligned to its element size; packed images
+// and workspaces to 256 bytes (what hipMalloc returns).
+bool aligned(const void* p, size_t a) { return (uintptr_t)p % a == 0; }
 
 }  // namespace
 
@@ -67,6 +70,7 @@ hd_status hd_encode(const void* X, const void* B, float* H, int64_t N, int64_t F
   if (!dims_ok(N, F, D, 1)) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!X || !B || !H) return HD_ERR_ARG;
+  if (!aligned(X, esize(dt)) || !aligned(B, esize(dt)) || !aligned(H, 4)) return HD_ERR_ARG;
   return from_hip(hd::launch_encode(X, B, H, N, F, D, dt, act, stream));
 }
 
@@ -76,6 +80,8 @@ hd_status hd_similarity(const float* H, const void* C, int32_t* labels, float* s
   if (!dims_ok(N, 1, D, K)) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!H || !C || !labels) return HD_ERR_ARG;
+  if (!aligned(H, 4) || !aligned(C, esize(c_dt)) || !aligned(labels, 4) || !aligned(scores, 4))
+    return HD_ERR_ARG;
   return from_hip(hd::launch_similarity(H, C, labels, scores, N, D, K, c_dt, stream));
 }
 
@@ -102,15 +108,12 @@ hd_status hd_pack_model(const void* B, const void* C, int64_t F, int64_t D, int6
   if (F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0)) return HD_ERR_ARG;
   if (!dims_ok(0, F, D, K)) return HD_ERR_UNSUPPORTED;
   if (!B || !C || !packed) return HD_ERR_ARG;
+  if (!aligned(B, esize(dt)) || !aligned(C, esize(dt)) || !aligned(packed, 256)) return HD_ERR_ARG;
   const Image im = image_layout(F, D, K, dt);
   if (packed_bytes < im.total) return HD_ERR_WORKSPACE;
   char* p = static_cast<char*>(packed);
   if (hd::launch_pack(B, C, F, D, K, dt, p, stream) != hipSuccess) return HD_ERR_HIP;
-  if (hipMemcpyAsync(p + im.tiled, B, (size_t)F * D * esize(dt), hipMemcpyDeviceToDevice,
-                     stream) != hipSuccess)
-    return HD_ERR_HIP;
-  if (hipMemcpyAsync(p + im.tiled + im.raw_b, C, (size_t)K * D * esize(dt),
-                     hipMemcpyDeviceToDevice, stream) != hipSuccess)
+  if (hd::launch_pack_small(B, C, F, D, K, dt, p + im.large, stream) != hipSuccess)
     return HD_ERR_HIP;
   return HD_OK;
 }
@@ -123,6 +126,10 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
   if (!dims_ok(N, F, D, K)) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!X || !labels || (packed ? false : (!B || !C))) return HD_ERR_ARG;
+  const size_t es = esize(dt);
+  if (!aligned(X, es) || !aligned(labels, 4) || !aligned(scores, 4) || !aligned(workspace, 256) ||
+      (packed ? !aligned(packed, 256) : (!aligned(B, es) || !aligned(C, es))))
+    return HD_ERR_ARG;
   const bool small = use_small(N, F, D, K, dt);
   if (!small && !hd::large_supported(N, F, D, K, dt)) return HD_ERR_UNSUPPORTED;
   const size_t need = packed ? hd_infer_packed_workspace_bytes(N, F, D, K, dt)
@@ -131,13 +138,9 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
   if (workspace_bytes < need) return HD_ERR_WORKSPACE;
 
   if (small) {
-    if (packed) {
-      const Image im = image_layout(F, D, K, dt);
-      B = static_cast<const char*>(packed) + im.tiled;
-      C = static_cast<const char*>(packed) + im.tiled + im.raw_b;
-    }
-    return from_hip(
-        hd::launch_small(X, B, C, labels, scores, N, F, D, K, dt, act, workspace, stream));
+    if (packed) B = static_cast<const char*>(packed) + image_layout(F, D, K, dt).large;
+    return from_hip(hd::launch_small(X, B, C, packed != nullptr, labels, scores, N, F, D, K, dt,
+                                     act, workspace, stream));
   }
   void* large_ws = workspace;
   if (!packed) {
@@ -156,6 +159,12 @@ hd_status hd_infer(const void* X, const void* B, const void* C, int32_t* labels,
                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
   return infer_common(X, B, C, nullptr, labels, scores, N, F, D, K, dt, act, workspace,
                       workspace_bytes, stream);
+}
+
+const char* hd_infer_kernel(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, int packed) {
+  if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return "";
+  if (use_small(N, F, D, K, dt)) return hd::small_kernel_name(N, F, D, K, dt, packed != 0);
+  return hd::large_supported(N, F, D, K, dt) ? "large_fused_kernel" : "";
 }
 
 hd_status hd_infer_packed(const void* X, const void* packed, int32_t* labels, float* scores,

@@ -13,7 +13,17 @@ constexpr int kSmallReplicas = 32;  // replicated score accumulators
 
 bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
-hipError_t launch_small(const void* X, const void* B, const void* C, int32_t* labels,
+// Name of the kernel launch_small would use for 16-byte aligned operands.
+const char* small_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled);
+
+// Bytes of the column-tiled model section the small-batch path reads from a
+// packed model, and the kernel that writes it.
+size_t small_packed_bytes(int64_t F, int64_t D, int64_t K, int dt);
+hipError_t launch_pack_small(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,
+                             void* out, hipStream_t stream);
+// tiled: B points at that section (C is then ignored); otherwise B and C are
+// the caller's row-major matrices.
+hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled, int32_t* labels,
                         float* scores, int64_t N, int64_t F, int64_t D, int64_t K, int dt,
                         int act, void* workspace, hipStream_t stream);
 

@@ -44,15 +44,23 @@ constexpr int kRG = kThreads / kCG;   // row groups (VALU kernel)
 constexpr int kRpt = 12;              // B rows per thread per chunk (VALU kernel)
 constexpr int kLdsBudget = 159 * 1024;
 
+// Workspace: the final ticket counter, kGroups group counters (each on its
+// own 256-byte line), then the R score replicas [R][N][K].
+constexpr int kGroups = 32;
+constexpr int kLine = 256;
+
 struct SmallWs {
   unsigned* counter;
-  float* sacc;  // [R][N][K]
+  unsigned* group;  // group g's counter at group + g * kLine / 4
+  float* sacc;      // [R][N][K]
 };
 
 __host__ __device__ inline SmallWs small_ws(void* ws) {
   SmallWs w;
-  w.counter = reinterpret_cast<unsigned*>(ws);
-  w.sacc = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + 256);
+  char* b = reinterpret_cast<char*>(ws);
+  w.counter = reinterpret_cast<unsigned*>(b);
+  w.group = reinterpret_cast<unsigned*>(b + kLine);
+  w.sacc = reinterpret_cast<float*>(b + kLine * (1 + kGroups));
   return w;
 }
 
@@ -87,44 +95,70 @@ __device__ __forceinline__ BlockWalk block_walk(int b, int G, int nblocks) {
   return w;
 }
 
-template <typename T>
-__device__ __forceinline__ float4 load_b4_vec(const T* __restrict__ B, int64_t row, int64_t col,
-                                              int64_t D) {
-  return load4(B, row * D + col);
-}
+// Where a column block's values live. Block blk covers columns 16 blk ..
+// 16 blk + 15 of a matrix with `rows` rows (B: F rows, C: K rows).
+//   kRawScalar / kRawVec: the caller's row-major matrix [rows][D]; columns
+//     past D are clamped into the row (their values are garbage and only meet
+//     zeroed encodings). kRawVec needs D % 4 == 0 and aligned bases, so a
+//     4-column group is either wholly inside the row or wholly past it.
+//   kTiled: the packed model's column-block layout [nblk][rows][16], zero past
+//     column D: one block is a single contiguous run, which keeps the DRAM
+//     access stream sequential (64-byte pieces of many rows are not).
+constexpr int kRawScalar = 0, kRawVec = 1, kTiled = 2;
 
-// Four elements at (row, col..col+3), columns clamped into the row. Values
-// for clamped columns are garbage; they only reach encoded columns >= D,
-// which are zeroed before Stage II.
-template <typename T>
-__device__ __forceinline__ float4 load_b4_any(const T* __restrict__ B, int64_t row, int64_t col,
-                                              int64_t D) {
-  float v[4];
+template <typename T, int LAY>
+struct ColView {
+  const T* __restrict__ p;
+  int64_t D;
+  int rows;
+  // B[r][16 blk + c .. +3]; c is a multiple of 4
+  __device__ __forceinline__ float4 get4(int blk, int r, int c) const {
+    if (LAY == kTiled) return load4(p, ((int64_t)blk * rows + r) * kW + c);
+    const int64_t col = (int64_t)blk * kW + c;
+    if (LAY == kRawVec) return load4(p, (int64_t)r * D + (col < D ? col : 0));
+    float v[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) v[q] = load_elem(B, row * D + (col + q < D ? col + q : D - 1));
-  return make_float4(v[0], v[1], v[2], v[3]);
-}
+    for (int q = 0; q < 4; ++q) v[q] = load_elem(p, (int64_t)r * D + (col + q < D ? col + q : D - 1));
+    return make_float4(v[0], v[1], v[2], v[3]);
+  }
+  __device__ __forceinline__ float get(int blk, int r, int c) const {
+    if (LAY == kTiled) return load_elem(p, ((int64_t)blk * rows + r) * kW + c);
+    const int64_t col = (int64_t)blk * kW + c;
+    return load_elem(p, (int64_t)r * D + (col < D ? col : D - 1));
+  }
+};
 
 // Copy the first n floats of X into LDS: 16-byte loads and stores, all of a
-// thread's loads in flight at once. X is 16-byte aligned (base of a tensor).
+// thread's loads in flight at once. X is 16-byte aligned. Stores are
+// unconditional (a branch per store lets the compiler sink each load to its
+// store, serialising them); threads past the end write the spare float4 slot
+// after the n floats, which the caller provides.
+__device__ __forceinline__ int x_rotation(int n4) {
+  // Every workgroup reads all of X. Starting each at a different 1 KiB
+  // offset spreads the simultaneous reads over the L2 channels instead of
+  // sending all of them to the channel holding the first bytes.
+  return n4 > 0 ? (int)(((int64_t)blockIdx.x * 37 * 64) % n4) : 0;
+}
+
 __device__ void copy_flat_to_lds(const float* __restrict__ X, float* xs, int n) {
   const int tid = threadIdx.x;
   const int n4 = n / 4;
+  const int rot = x_rotation(n4);
   const float4* src = reinterpret_cast<const float4*>(X);
   float4* dst = reinterpret_cast<float4*>(xs);
   constexpr int kBatch = 24;
   for (int base = 0; base < n4; base += kThreads * kBatch) {
     float4 v[kBatch];
+    int at[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const int i = base + j * kThreads + tid;
-      v[j] = src[i < n4 ? i : 0];
+      const int r = i + rot >= n4 ? i + rot - n4 : i + rot;
+      at[j] = i < n4 ? r : n4;
+      v[j] = src[i < n4 ? r : 0];
     }
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const int i = base + j * kThreads + tid;
-      if (i < n4) dst[i] = v[j];
-    }
+    for (int j = 0; j < kBatch; ++j) dst[at[j]] = v[j];
   }
   for (int i = 4 * n4 + tid; i < n; i += kThreads) xs[i] = X[i];
 }
@@ -140,39 +174,32 @@ __device__ void stage_rows_chunk(const T* __restrict__ X, float* xs, int Pf, int
   }
 }
 
-// The 16 C values C[k][d0..d0+15] of (sample, class) pair p = threadIdx.x,
-// loaded unconditionally with clamped addresses so the load count per thread
-// is fixed. No select is applied to the loaded values (that would force a
-// wait right here): pairs past N*K are never used and columns past D meet
-// zeroed encoded values.
-template <typename T>
-__device__ __forceinline__ void load_c_pair(const T* __restrict__ C, int K, int64_t D, int64_t d0,
-                                            int npairs, float (&c)[kW]) {
+// The 16 C values C[k][16 blk .. 16 blk + 15] of (sample, class) pair
+// p = threadIdx.x, loaded unconditionally with clamped addresses so the load
+// count per thread is fixed. No select is applied to the loaded values (that
+// would force a wait right here): pairs past N*K are never used and columns
+// past D meet zeroed encoded values.
+template <typename T, int LAY>
+__device__ __forceinline__ void load_c_pair(const ColView<T, LAY>& cv, int K, int blk, int npairs,
+                                            float (&c)[kW]) {
   const int p = threadIdx.x;
   const int k = p < npairs ? p % K : 0;
-  const T* crow = C + (int64_t)k * D;
-  if ((D & 15) == 0) {
-    // the block is 16 whole, aligned elements of the row: 4-element loads
 #pragma unroll
-    for (int j = 0; j < kW; j += 4) {
-      const float4 v = load4(crow, d0 + j);
-      c[j] = v.x;
-      c[j + 1] = v.y;
-      c[j + 2] = v.z;
-      c[j + 3] = v.w;
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < kW; ++j) c[j] = load_elem(crow, d0 + j < D ? d0 + j : D - 1);
+  for (int j = 0; j < kW; j += 4) {
+    const float4 v = cv.get4(blk, k, j);
+    c[j] = v.x;
+    c[j + 1] = v.y;
+    c[j + 2] = v.z;
+    c[j + 3] = v.w;
   }
 }
 
 // Partial similarity of one finished block: sl[n*K + k] += sum_c hs[n][c] C[k][d0+c]
 // (Eq. 8 restricted to the block's columns). hs is [NB][kW+1]; pair
 // threadIdx.x uses the preloaded cpair, further pairs read C directly.
-template <typename T>
-__device__ void block_scores(const T* __restrict__ C, const float* hs, float* sl, int npairs, int K,
-                             int64_t D, int64_t d0, const float (&cpair)[kW]) {
+template <typename T, int LAY>
+__device__ void block_scores(const ColView<T, LAY>& cv, const float* hs, float* sl, int npairs,
+                             int K, int blk, const float (&cpair)[kW]) {
   const int tid = threadIdx.x;
   if (tid < npairs) {
     const int n = tid / K;
@@ -183,9 +210,9 @@ __device__ void block_scores(const T* __restrict__ C, const float* hs, float* sl
   }
   for (int p = tid + kThreads; p < npairs; p += kThreads) {
     const int n = p / K, k = p - n * K;
-    const T* crow = C + (int64_t)k * D;
     float s = 0.0f;
-    for (int j = 0; j < kW && d0 + j < D; ++j) s = fmaf(hs[n * (kW + 1) + j], load_elem(crow, d0 + j), s);
+#pragma unroll
+    for (int j = 0; j < kW; ++j) s = fmaf(hs[n * (kW + 1) + j], cv.get(blk, k, j), s);
     sl[p] += s;
   }
 }
@@ -193,6 +220,13 @@ __device__ void block_scores(const T* __restrict__ C, const float* hs, float* sl
 // Publish this workgroup's partial scores (samples [nb0, nb0+nb)); after the
 // last sample block, take a ticket and, in the last workgroup, finish: sum
 // the replicas, write scores and labels, and re-zero the ticket.
+//
+// Tickets are drawn in two levels. Atomics on one address are performed one
+// after another (about 10 ns each), so a single counter drawn by hundreds of
+// workgroups would serialise for microseconds. Workgroup b draws from group
+// counter b % kGroups; the group's last drawer (which then knows that every
+// member's partials are performed) resets it and draws from the final
+// counter; the last of those finishes.
 __device__ void publish_and_finish(const float* sl, int nb0, int nb, int N, int K, int R,
                                    const SmallWs& ws, int32_t* __restrict__ labels,
                                    float* __restrict__ scores, float* buf, int buf_floats,
@@ -204,7 +238,17 @@ __device__ void publish_and_finish(const float* sl, int nb0, int nb, int N, int 
   __shared__ int s_last;
   wait_own_memory_ops();
   __syncthreads();
-  if (tid == 0) s_last = (take_ticket(ws.counter) == gridDim.x - 1) ? 1 : 0;
+  if (tid == 0) {
+    const unsigned G = gridDim.x, ng = G < kGroups ? G : kGroups, g = blockIdx.x % ng;
+    const unsigned gsize = G / ng + (g < G % ng ? 1u : 0u);
+    unsigned* gc = ws.group + g * (kLine / 4);
+    int last = 0;
+    if (take_ticket(gc) == gsize - 1) {
+      reset_counter(gc);
+      last = take_ticket(ws.counter) == ng - 1 ? 1 : 0;
+    }
+    s_last = last;
+  }
   __syncthreads();
   if (!s_last) return;
   const int64_t NK = (int64_t)N * K;
@@ -332,7 +376,7 @@ struct ValuBuf {
   float c[kW];
 };
 
-template <typename T, int NB, bool VEC>
+template <typename T, int NB, int LAY>
 __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
     const T* __restrict__ X, const T* __restrict__ B, const T* __restrict__ C,
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
@@ -345,6 +389,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
   float* hs = red + kWaves * 4 * NB * kW;
   float* sl = hs + NB * (kW + 1);
   const SmallWs ws = small_ws(workspace);
+  const ColView<T, LAY> bv{B, D, F}, cv{C, D, K};
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int cg = tid % kCG, rg = tid / kCG;
   const int G = gridDim.x;
@@ -361,7 +406,6 @@ __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
     // Items are (block, chunk) pairs in this workgroup's order.
     auto load = [&](ValuBuf<T, NB>& x, int it) {
       const int blk = walk.block_of(it / nchunks), ch = it % nchunks;
-      const int64_t col = (int64_t)blk * kW + cg * 4;
       const int f0 = ch * FC, fcn = min(FC, F - f0);
 #pragma unroll
       for (int u = 0; u < kRpt; ++u) {
@@ -369,10 +413,9 @@ __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
         // is skipped); columns past D give garbage zeroed after encoding
         const int f = rg + kRG * u;
         const int fc = f < fcn ? f : fcn - 1;
-        x.b[u] = VEC ? load_b4_vec(B, f0 + fc, col < D ? col : 0, D)
-                     : load_b4_any(B, f0 + fc, col, D);
+        x.b[u] = bv.get4(blk, f0 + fc, cg * 4);
       }
-      load_c_pair(C, K, D, (int64_t)blk * kW, npairs, x.c);
+      load_c_pair(cv, K, blk, npairs, x.c);
     };
 
     ValuBuf<T, NB> b0, b1, b2;
@@ -451,7 +494,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
         hs[n * (kW + 1) + c] = (d0 + c < D && n < nb) ? activate(v, act) : 0.0f;
       }
       __syncthreads();
-      block_scores(C, hs, sl, npairs, K, D, d0, x.c);
+      block_scores(cv, hs, sl, npairs, K, blk, x.c);
     };
 
     ring3_run(nitems, b0, b1, b2, load, process);
@@ -477,7 +520,7 @@ struct MfmaBuf {
   float c[kW];
 };
 
-template <int NTI, int MS>
+template <int NTI, int MS, int LAY>
 __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
     const float* __restrict__ X, const float* __restrict__ B, const float* __restrict__ C,
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
@@ -490,6 +533,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
   float* hs = red + kWaves * NTI * 256;            // [NB][17]
   float* xs = red;  // [nb][F]: X rows, only until the operands are in registers
   const SmallWs ws = small_ws(workspace);
+  const ColView<float, LAY> bv{B, D, F}, cv{C, D, K};
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = gridDim.x;
   const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
@@ -501,16 +545,15 @@ __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
   const int nmine = walk.count();
 
   auto load = [&](MfmaBuf<MS>& x, int i) {
-    const int64_t col = (int64_t)walk.block_of(i) * kW + acol;
-    const int64_t cc = col < D ? col : D - 1;
+    const int blk = walk.block_of(i);
 #pragma unroll
     for (int s = 0; s < MS; ++s) {
       // rows past F are clamped and meet zero X values; columns past D give
       // garbage that is zeroed after encoding
       const int f = arow + 4 * s;
-      x.a[s] = B[(int64_t)(f < F ? f : F - 1) * D + cc];
+      x.a[s] = bv.get(blk, f < F ? f : F - 1, acol);
     }
-    load_c_pair(C, K, D, (int64_t)walk.block_of(i) * kW, npairs, x.c);
+    load_c_pair(cv, K, blk, npairs, x.c);
   };
 
   // B is in flight while X (rows 0..nb-1, one contiguous range) is copied to
@@ -531,7 +574,8 @@ __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
     }
 
   auto process = [&](const MfmaBuf<MS>& x, int i) {
-    const int64_t d0 = (int64_t)walk.block_of(i) * kW;
+    const int blk = walk.block_of(i);
+    const int64_t d0 = (int64_t)blk * kW;
     f32x4 acc[NTI];
 #pragma unroll
     for (int t = 0; t < NTI; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -556,7 +600,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
       hs[n * (kW + 1) + c] = (d0 + c < D && n < nb) ? activate(v, act) : 0.0f;
     }
     __syncthreads();
-    block_scores(C, hs, sl, npairs, K, D, d0, x.c);
+    block_scores(cv, hs, sl, npairs, K, blk, x.c);
   };
 
   ring3_run(nmine, b0, b1, b2, load, process);
@@ -578,7 +622,7 @@ __device__ __forceinline__ int xcd_block(int b, int G) {
   return x * per + min(x, rem) + j;
 }
 
-template <typename T, int NB, int RPT, bool VEC>
+template <typename T, int NB, int RPT, int LAY>
 __global__ __launch_bounds__(kThreads) void small_flat_kernel(
     const T* __restrict__ X, const T* __restrict__ B, const T* __restrict__ C,
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
@@ -587,18 +631,17 @@ __global__ __launch_bounds__(kThreads) void small_flat_kernel(
   __shared__ float red[kWaves * 4 * NB * kW];
   __shared__ float hs[NB * (kW + 1)];
   const SmallWs ws = small_ws(workspace);
+  const ColView<T, LAY> bv{B, D, F}, cv{C, D, K};
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int cg = tid % kCG, rg = tid / kCG;
   const int G = gridDim.x;
   const int blk = xcd_block(blockIdx.x, G);
   const int R = replicas(G);
   const int64_t d0 = (int64_t)blk * kW;
-  const int64_t col = d0 + cg * 4;
-  const int64_t colc = col < D ? col : 0;
   const int npairs = N * K;
 
   float cpair[kW];
-  load_c_pair(C, K, D, d0, npairs, cpair);
+  load_c_pair(cv, K, blk, npairs, cpair);
   float acc[NB][4];
 #pragma unroll
   for (int n = 0; n < NB; ++n) acc[n][0] = acc[n][1] = acc[n][2] = acc[n][3] = 0.0f;
@@ -611,7 +654,7 @@ __global__ __launch_bounds__(kThreads) void small_flat_kernel(
       // give garbage that is zeroed after encoding
       const int f = f0 + rg + kRG * u;
       const int fc = f < F ? f : F - 1;
-      b[u] = VEC ? load_b4_vec(B, fc, colc, D) : load_b4_any(B, fc, col, D);
+      b[u] = bv.get4(blk, fc, cg * 4);
     }
 #pragma unroll
     for (int u = 0; u < RPT; ++u) {
@@ -660,13 +703,134 @@ __global__ __launch_bounds__(kThreads) void small_flat_kernel(
   }
   for (int p = tid + kThreads; p < npairs; p += kThreads) {
     const int n = p / K, k = p - n * K;
-    const T* crow = C + (int64_t)k * D;
     float sc = 0.0f;
-    for (int j = 0; j < kW && d0 + j < D; ++j) sc = fmaf(hs[n * (kW + 1) + j], load_elem(crow, d0 + j), sc);
+#pragma unroll
+    for (int j = 0; j < kW; ++j) sc = fmaf(hs[n * (kW + 1) + j], cv.get(blk, k, j), sc);
     publish_add(my + p, sc);
   }
   float none[1] = {0.0f};
   publish_and_finish(none, 0, 0, N, K, R, ws, labels, scores, red, kWaves * 4 * NB * kW, true);
+}
+
+// ---------------------------------------------------------------------------
+// Block matrix-core kernel (fp32, 8 < N <= 32, one column block per
+// workgroup). Same operand mapping as small_mfma_kernel; X (all nb rows, one
+// contiguous range) is loaded first, since it is shared by every workgroup
+// and hits L2, then the block's B rows and C values, so the X wait does not
+// wait for B. X passes through LDS into registers; the LDS then holds the
+// wave partials.
+// LDS: xs[nb][F] during staging, then red[4][NTI][256] | hs[16*NTI][17]
+// ---------------------------------------------------------------------------
+template <int NTI, int MS, int LAY>
+__global__ __launch_bounds__(kThreads) void small_block_mfma_kernel(
+    const float* __restrict__ X, const float* __restrict__ B, const float* __restrict__ C,
+    int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
+    int lds_floats, void* __restrict__ workspace) {
+  constexpr int NB = 16 * NTI;
+  constexpr int FQ = 4 * MS;  // rows per wave
+  constexpr int XV = NTI * MS / 4;  // float4 of X per thread: 16 NTI rows of up to 16 MS
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  float* xs = smem;
+  float* red = smem;
+  float* hs = red + kWaves * NTI * 256;
+  const SmallWs ws = small_ws(workspace);
+  const ColView<float, LAY> bv{B, D, F}, cv{C, D, K};
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int G = gridDim.x;
+  const int blk = xcd_block(blockIdx.x, G);
+  const int R = replicas(G);
+  const int nb = min(NB, N);
+  const int npairs = nb * K;
+  const int arow = wave * FQ + (lane >> 4);
+  const int acol = lane & 15;
+  const int64_t d0 = (int64_t)blk * kW;
+
+  // 1. X: XV float4 per thread, addresses clamped
+  const int n4 = nb * F / 4;
+  const int rot = x_rotation(n4);
+  const float4* x4 = reinterpret_cast<const float4*>(X);
+  float4 xv[XV];
+  int at[XV];
+#pragma unroll
+  for (int j = 0; j < XV; ++j) {
+    const int i = j * kThreads + tid;
+    const int r = i + rot >= n4 ? i + rot - n4 : i + rot;
+    at[j] = i < n4 ? r : n4;
+    xv[j] = x4[i < n4 ? r : 0];
+  }
+  // keep the X loads ahead of the B loads (the wait for X must not wait for B)
+  __builtin_amdgcn_sched_barrier(0);
+  // 2. B rows (A operand) and the pair's C values
+  float a[MS];
+#pragma unroll
+  for (int s = 0; s < MS; ++s) {
+    // rows past F are clamped and meet zero X values; columns past D give
+    // garbage that is zeroed after encoding
+    const int f = arow + 4 * s;
+    a[s] = bv.get(blk, f < F ? f : F - 1, acol);
+  }
+  float cpair[kW];
+  load_c_pair(cv, K, blk, npairs, cpair);
+
+  // 3. X to LDS, then the wave's operand values to registers. Stores are
+  // unconditional (a branch per store lets the compiler sink each load to its
+  // store); threads past the end write the spare slot after X.
+#pragma unroll
+  for (int j = 0; j < XV; ++j) reinterpret_cast<float4*>(xs)[at[j]] = xv[j];
+  for (int i = 4 * n4 + tid; i < nb * F; i += kThreads) xs[i] = X[i];
+  __syncthreads();
+  float xr[MS][NTI];
+#pragma unroll
+  for (int s = 0; s < MS; ++s)
+#pragma unroll
+    for (int t = 0; t < NTI; ++t) {
+      const int n = 16 * t + (lane & 15), f = arow + 4 * s;
+      const float v = xs[(n < nb ? n : 0) * F + (f < F ? f : 0)];
+      xr[s][t] = (n < nb && f < F) ? v : 0.0f;
+    }
+
+  // 4. V^T tiles over the wave's rows, summed over the waves through LDS
+  f32x4 acc[NTI];
+#pragma unroll
+  for (int t = 0; t < NTI; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < MS; ++s)
+#pragma unroll
+    for (int t = 0; t < NTI; ++t)
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], xr[s][t], acc[t], 0, 0, 0);
+  __syncthreads();  // every wave has read its X values: xs becomes red
+#pragma unroll
+  for (int t = 0; t < NTI; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      red[(wave * NTI + t) * 256 + (4 * (lane >> 4) + r) * 16 + (lane & 15)] = acc[t][r];
+  __syncthreads();
+  for (int e = tid; e < NB * kW; e += kThreads) {
+    const int n = e / kW, c = e % kW;
+    const int t = n / 16, j = n % 16;
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) v += red[(w * NTI + t) * 256 + c * 16 + j];
+    hs[n * (kW + 1) + c] = (d0 + c < D && n < nb) ? activate(v, act) : 0.0f;
+  }
+  __syncthreads();
+
+  // 5. partial scores of this block straight to the replica
+  float* my = ws.sacc + (int64_t)(blockIdx.x % R) * N * K;
+  for (int p = tid; p < npairs; p += kThreads) {
+    const int n = p / K, k = p - n * K;
+    float sc = 0.0f;
+    if (p == tid) {
+#pragma unroll
+      for (int j = 0; j < kW; ++j) sc = fmaf(hs[n * (kW + 1) + j], cpair[j], sc);
+    } else {
+#pragma unroll
+      for (int j = 0; j < kW; ++j) sc = fmaf(hs[n * (kW + 1) + j], cv.get(blk, k, j), sc);
+    }
+    publish_add(my + p, sc);
+  }
+  float none[1] = {0.0f};
+  publish_and_finish(none, 0, 0, N, K, R, ws, labels, scores, smem, lds_floats, true);
 }
 
 int num_cus() {
@@ -686,6 +850,7 @@ constexpr int kMfmaSteps[] = {12, 24, 36, 48};  // 4-row steps per wave: F <= 16
 struct SmallPlan {
   bool flat;  // one block per workgroup (N <= 8)
   int rpt;    // flat kernel: rows per thread per chunk
+  bool bmfma;  // block matrix-core kernel (one block per workgroup, N <= 32)
   bool mfma;
   int nb;    // VALU samples per pass, or MFMA sample tiles
   int ms;    // MFMA steps per wave
@@ -695,38 +860,16 @@ struct SmallPlan {
   int nblocks;
 };
 
-SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+// The VALU kernel serves every layout and alignment; it is the support
+// criterion. Returns nb == 0 when nb * K does not fit in LDS.
+SmallPlan plan_valu(int64_t N, int64_t F, int64_t D, int64_t K) {
   SmallPlan p{};
   p.nblocks = (int)cdiv(D, kW);
-  if (N <= 8) {
-    p.flat = true;
-    p.nb = N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : 8;
-    p.rpt = F <= kRG * 4 ? 4 : F <= kRG * 6 ? 6 : F <= kRG * 9 ? 9 : F <= kRG * 12 ? 12 : 16;
-    p.grid = p.nblocks;
-    return p;
-  }
   p.grid = p.nblocks < num_cus() ? p.nblocks : num_cus();
-  const int nti = (int)cdiv(N, 16);
-  if (dt == 0 && N > 8) {
-    for (int ms : kMfmaSteps) {
-      if ((int64_t)16 * ms < F) continue;
-      const int64_t scratch = kWaves * nti * 256 + 16 * nti * (kW + 1);
-      const int64_t lds = (int64_t)sizeof(float) *
-                          ((16 * nti * K + 3) / 4 * 4 + (scratch > N * F ? scratch : N * F));
-      if (lds <= kLdsBudget) {
-        p.mfma = true;
-        p.nb = nti;
-        p.ms = ms;
-        p.lds = (size_t)lds;
-        return p;
-      }
-      break;
-    }
-  }
   const int nb = N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : N <= 8 ? 8 : N <= 16 ? 16 : 32;
   const int64_t fixed =
       (int64_t)sizeof(float) * (kWaves * 4 * nb * kW + nb * (kW + 1) + nb * K);
-  if (fixed > kLdsBudget) return p;  // nb * K too large for LDS: unsupported
+  if (fixed > kLdsBudget) return p;
   if (F <= kRG * kRpt) {
     p.FC = (int)F;  // one chunk: X lives in registers, no staging area
     p.lds = (size_t)fixed;
@@ -739,6 +882,59 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   }
   p.nb = nb;
   return p;
+}
+
+// Kernel choice: N <= 8 takes the flat kernel, fp32 with 8 < N <= 64 the
+// matrix-core kernel when its LDS fits; raw matrices with unaligned bases or
+// D % 4 != 0 (kRawScalar) and everything else take the VALU kernel.
+SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay, bool x_aligned) {
+  SmallPlan v = plan_valu(N, F, D, K);
+  if (v.nb == 0 || lay == kRawScalar) return v;
+  SmallPlan p{};
+  p.nblocks = v.nblocks;
+  if (N <= 8) {
+    p.flat = true;
+    p.nb = N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : 8;
+    p.rpt = F <= kRG * 4 ? 4 : F <= kRG * 9 ? 9 : 16;
+    p.grid = p.nblocks;
+    return p;
+  }
+  if (dt == 0 && x_aligned && N <= 32) {
+    const int nti = (int)cdiv(N, 16);
+    for (int ms : kMfmaSteps) {
+      if ((int64_t)16 * ms < F) continue;
+      const int64_t red = kWaves * nti * 256 + 16 * nti * (kW + 1);
+      const int64_t xs = N * F + 4;  // X and one spare float4
+      const int64_t lds = (int64_t)sizeof(float) * (red > xs ? red : xs);
+      if (lds > kLdsBudget) break;
+      p.bmfma = true;
+      p.nb = nti;
+      p.ms = ms;
+      p.lds = (size_t)lds;
+      p.grid = p.nblocks;
+      return p;
+    }
+  }
+  if (dt == 0 && x_aligned) {
+    const int nti = (int)cdiv(N, 16);
+    for (int ms : kMfmaSteps) {
+      if ((int64_t)16 * ms < F) continue;
+      const int64_t scratch = kWaves * nti * 256 + 16 * nti * (kW + 1);
+      const int64_t xs = N * F + 4;  // X and one spare float4
+      const int64_t lds = (int64_t)sizeof(float) *
+                          ((16 * nti * K + 3) / 4 * 4 + (scratch > xs ? scratch : xs));
+      if (lds <= kLdsBudget) {
+        p.mfma = true;
+        p.nb = nti;
+        p.ms = ms;
+        p.lds = (size_t)lds;
+        p.grid = v.grid;
+        return p;
+      }
+      break;
+    }
+  }
+  return v;
 }
 
 // The last workgroup reuses all of LDS to sum the R score replicas, so give
@@ -754,133 +950,220 @@ hipError_t allow_lds(KernelT* k) {
                              hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget);
 }
 
-template <typename T, int NB, bool VEC>
-hipError_t launch_valu(const SmallPlan& p, const void* X, const void* B, const void* C,
-                       int32_t* labels, float* scores, int N, int F, int D, int K, int act,
-                       void* ws, hipStream_t stream) {
-  static const hipError_t attr = allow_lds(&small_valu_kernel<T, NB, VEC>);
+struct Args {
+  const void *X, *B, *C;
+  int32_t* labels;
+  float* scores;
+  int N, F, D, K, act;
+  void* ws;
+  hipStream_t stream;
+};
+
+template <typename T, int NB, int LAY>
+hipError_t launch_valu(const SmallPlan& p, const Args& a) {
+  static const hipError_t attr = allow_lds(&small_valu_kernel<T, NB, LAY>);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((small_valu_kernel<T, NB, VEC>), dim3(p.grid), dim3(kThreads), p.lds, stream,
-                     (const T*)X, (const T*)B, (const T*)C, labels, scores, N, F, D, K, act, p.FC,
-                     p.nblocks, (int)(p.lds / sizeof(float)), ws);
+  hipLaunchKernelGGL((small_valu_kernel<T, NB, LAY>), dim3(p.grid), dim3(kThreads), p.lds,
+                     a.stream, (const T*)a.X, (const T*)a.B, (const T*)a.C, a.labels, a.scores,
+                     a.N, a.F, a.D, a.K, a.act, p.FC, p.nblocks, (int)(p.lds / sizeof(float)),
+                     a.ws);
   return hipGetLastError();
 }
 
-template <int NTI, int MS>
-hipError_t launch_mfma(const SmallPlan& p, const void* X, const void* B, const void* C,
-                       int32_t* labels, float* scores, int N, int F, int D, int K, int act,
-                       void* ws, hipStream_t stream) {
-  static const hipError_t attr = allow_lds(&small_mfma_kernel<NTI, MS>);
-  if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((small_mfma_kernel<NTI, MS>), dim3(p.grid), dim3(kThreads), p.lds, stream,
-                     (const float*)X, (const float*)B, (const float*)C, labels, scores, N, F, D, K,
-                     act, p.nblocks, (int)(p.lds / sizeof(float)), ws);
-  return hipGetLastError();
-}
-
-template <int NTI>
-hipError_t launch_mfma_ms(const SmallPlan& p, const void* X, const void* B, const void* C,
-                          int32_t* labels, float* scores, int N, int F, int D, int K, int act,
-                          void* ws, hipStream_t stream) {
-  switch (p.ms) {
-    case 12: return launch_mfma<NTI, 12>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 24: return launch_mfma<NTI, 24>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 36: return launch_mfma<NTI, 36>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    default: return launch_mfma<NTI, 48>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-  }
-}
-
-template <typename T, bool VEC>
-hipError_t launch_valu_t(const SmallPlan& p, const void* X, const void* B, const void* C,
-                         int32_t* labels, float* scores, int N, int F, int D, int K, int act,
-                         void* ws, hipStream_t stream) {
+template <typename T, int LAY>
+hipError_t launch_valu_nb(const SmallPlan& p, const Args& a) {
   switch (p.nb) {
-    case 1: return launch_valu<T, 1, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 2: return launch_valu<T, 2, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 4: return launch_valu<T, 4, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 8: return launch_valu<T, 8, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 16: return launch_valu<T, 16, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    default: return launch_valu<T, 32, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
+    case 1: return launch_valu<T, 1, LAY>(p, a);
+    case 2: return launch_valu<T, 2, LAY>(p, a);
+    case 4: return launch_valu<T, 4, LAY>(p, a);
+    case 8: return launch_valu<T, 8, LAY>(p, a);
+    case 16: return launch_valu<T, 16, LAY>(p, a);
+    default: return launch_valu<T, 32, LAY>(p, a);
   }
+}
+
+template <int NTI, int MS, int LAY>
+hipError_t launch_mfma(const SmallPlan& p, const Args& a) {
+  static const hipError_t attr = allow_lds(&small_mfma_kernel<NTI, MS, LAY>);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((small_mfma_kernel<NTI, MS, LAY>), dim3(p.grid), dim3(kThreads), p.lds,
+                     a.stream, (const float*)a.X, (const float*)a.B, (const float*)a.C, a.labels,
+                     a.scores, a.N, a.F, a.D, a.K, a.act, p.nblocks, (int)(p.lds / sizeof(float)),
+                     a.ws);
+  return hipGetLastError();
+}
+
+template <int NTI, int LAY>
+hipError_t launch_mfma_ms(const SmallPlan& p, const Args& a) {
+  switch (p.ms) {
+    case 12: return launch_mfma<NTI, 12, LAY>(p, a);
+    case 24: return launch_mfma<NTI, 24, LAY>(p, a);
+    case 36: return launch_mfma<NTI, 36, LAY>(p, a);
+    default: return launch_mfma<NTI, 48, LAY>(p, a);
+  }
+}
+
+template <int NTI, int MS, int LAY>
+hipError_t launch_bmfma(const SmallPlan& p, const Args& a) {
+  static const hipError_t attr = allow_lds(&small_block_mfma_kernel<NTI, MS, LAY>);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((small_block_mfma_kernel<NTI, MS, LAY>), dim3(p.grid), dim3(kThreads), p.lds,
+                     a.stream, (const float*)a.X, (const float*)a.B, (const float*)a.C, a.labels,
+                     a.scores, a.N, a.F, a.D, a.K, a.act, (int)(p.lds / sizeof(float)), a.ws);
+  return hipGetLastError();
+}
+
+template <int NTI, int LAY>
+hipError_t launch_bmfma_ms(const SmallPlan& p, const Args& a) {
+  switch (p.ms) {
+    case 12: return launch_bmfma<NTI, 12, LAY>(p, a);
+    case 24: return launch_bmfma<NTI, 24, LAY>(p, a);
+    case 36: return launch_bmfma<NTI, 36, LAY>(p, a);
+    default: return launch_bmfma<NTI, 48, LAY>(p, a);
+  }
+}
+
+template <int LAY>
+hipError_t launch_mfma_nti(const SmallPlan& p, const Args& a) {
+  switch (p.nb) {
+    case 1: return launch_mfma_ms<1, LAY>(p, a);
+    case 2: return launch_mfma_ms<2, LAY>(p, a);
+    case 3: return launch_mfma_ms<3, LAY>(p, a);
+    default: return launch_mfma_ms<4, LAY>(p, a);
+  }
+}
+
+template <typename T, int NB, int RPT, int LAY>
+hipError_t launch_flat(const SmallPlan& p, const Args& a) {
+  hipLaunchKernelGGL((small_flat_kernel<T, NB, RPT, LAY>), dim3(p.grid), dim3(kThreads), 0,
+                     a.stream, (const T*)a.X, (const T*)a.B, (const T*)a.C, a.labels, a.scores,
+                     a.N, a.F, a.D, a.K, a.act, a.ws);
+  return hipGetLastError();
+}
+
+template <typename T, int NB, int LAY>
+hipError_t launch_flat_rpt(const SmallPlan& p, const Args& a) {
+  switch (p.rpt) {
+    case 4: return launch_flat<T, NB, 4, LAY>(p, a);
+    case 9: return launch_flat<T, NB, 9, LAY>(p, a);
+    default: return launch_flat<T, NB, 16, LAY>(p, a);
+  }
+}
+
+template <typename T, int LAY>
+hipError_t launch_flat_nb(const SmallPlan& p, const Args& a) {
+  switch (p.nb) {
+    case 1: return launch_flat_rpt<T, 1, LAY>(p, a);
+    case 2: return launch_flat_rpt<T, 2, LAY>(p, a);
+    case 4: return launch_flat_rpt<T, 4, LAY>(p, a);
+    default: return launch_flat_rpt<T, 8, LAY>(p, a);
+  }
+}
+
+template <typename T, int LAY>
+hipError_t launch_plan(SmallPlan& p, const Args& a) {
+  if constexpr (LAY != kRawScalar) {
+    if (p.flat) return launch_flat_nb<T, LAY>(p, a);
+    if constexpr (sizeof(T) == 4) {
+      if (p.bmfma) {
+        widen_for_final(p, a.N, a.K);
+        return p.nb == 1 ? launch_bmfma_ms<1, LAY>(p, a) : launch_bmfma_ms<2, LAY>(p, a);
+      }
+      if (p.mfma) {
+        widen_for_final(p, a.N, a.K);
+        return launch_mfma_nti<LAY>(p, a);
+      }
+    }
+  }
+  widen_for_final(p, a.N, a.K);
+  return launch_valu_nb<T, LAY>(p, a);
+}
+
+template <typename T>
+hipError_t launch_t(SmallPlan& p, int lay, const Args& a) {
+  switch (lay) {
+    case kTiled: return launch_plan<T, kTiled>(p, a);
+    case kRawVec: return launch_plan<T, kRawVec>(p, a);
+    default: return launch_plan<T, kRawScalar>(p, a);
+  }
+}
+
+// Small-batch column-tiled model image: B as [nblk][F][16], then C as
+// [nblk][K][16] (each section starting on a 256-byte boundary), zero past
+// column D.
+template <typename T>
+__global__ __launch_bounds__(256) void pack_small_kernel(const T* __restrict__ src,
+                                                         T* __restrict__ dst, int64_t rows,
+                                                         int64_t D, int64_t nblk) {
+  const int64_t total = nblk * rows * kW;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * 256) {
+    const int64_t c = i % kW, r = (i / kW) % rows, blk = i / (kW * rows);
+    const int64_t col = blk * kW + c;
+    dst[i] = col < D ? src[r * D + col] : T(0);
+  }
+}
+
+template <typename T>
+hipError_t pack_small_t(const void* B, const void* C, int64_t F, int64_t D, int64_t K,
+                        void* out, hipStream_t stream) {
+  const int64_t nblk = cdiv(D, kW);
+  T* b = static_cast<T*>(out);
+  T* c = reinterpret_cast<T*>(static_cast<char*>(out) + (nblk * F * kW * sizeof(T) + 255) / 256 * 256);
+  const int64_t gb = cdiv(nblk * F * kW, 256), gc = cdiv(nblk * K * kW, 256);
+  hipLaunchKernelGGL(pack_small_kernel<T>, dim3((unsigned)(gb < 65536 ? gb : 65536)), dim3(256), 0,
+                     stream, (const T*)B, b, F, D, nblk);
+  hipLaunchKernelGGL(pack_small_kernel<T>, dim3((unsigned)(gc < 65536 ? gc : 65536)), dim3(256), 0,
+                     stream, (const T*)C, c, K, D, nblk);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  return plan_small(N, F, D, K, dt).nb > 0;
+  return plan_valu(N, F, D, K).nb > 0;
 }
 
 size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  const SmallPlan p = plan_small(N, F, D, K, dt);
-  return 256 + sizeof(float) * (size_t)replicas(p.grid) * N * K;
+  return (size_t)kLine * (1 + kGroups) + sizeof(float) * (size_t)kSmallReplicas * N * K;
 }
 
-template <typename T, int NB, int RPT, bool VEC>
-hipError_t launch_flat(const SmallPlan& p, const void* X, const void* B, const void* C,
-                       int32_t* labels, float* scores, int N, int F, int D, int K, int act,
-                       void* ws, hipStream_t stream) {
-  hipLaunchKernelGGL((small_flat_kernel<T, NB, RPT, VEC>), dim3(p.grid), dim3(kThreads), 0, stream,
-                     (const T*)X, (const T*)B, (const T*)C, labels, scores, N, F, D, K, act, ws);
-  return hipGetLastError();
+const char* small_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
+  const SmallPlan p = plan_small(N, F, D, K, dt, tiled ? kTiled : kRawVec, true);
+  if (p.nb == 0) return "";
+  return p.flat ? "small_flat_kernel" : p.bmfma ? "small_block_mfma_kernel"
+                                      : p.mfma  ? "small_mfma_kernel" : "small_valu_kernel";
 }
 
-template <typename T, int NB, bool VEC>
-hipError_t launch_flat_rpt(const SmallPlan& p, const void* X, const void* B, const void* C,
-                           int32_t* labels, float* scores, int N, int F, int D, int K, int act,
-                           void* ws, hipStream_t stream) {
-  switch (p.rpt) {
-    case 4: return launch_flat<T, NB, 4, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 6: return launch_flat<T, NB, 6, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 9: return launch_flat<T, NB, 9, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 12: return launch_flat<T, NB, 12, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    default: return launch_flat<T, NB, 16, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-  }
+size_t small_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {
+  const size_t es = dt == 0 ? 4 : 2;
+  const size_t nblk = (size_t)cdiv(D, kW);
+  return (nblk * F * kW * es + 255) / 256 * 256 + (nblk * K * kW * es + 255) / 256 * 256;
 }
 
-template <typename T, bool VEC>
-hipError_t launch_flat_t(const SmallPlan& p, const void* X, const void* B, const void* C,
-                         int32_t* labels, float* scores, int N, int F, int D, int K, int act,
-                         void* ws, hipStream_t stream) {
-  switch (p.nb) {
-    case 1: return launch_flat_rpt<T, 1, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 2: return launch_flat_rpt<T, 2, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    case 4: return launch_flat_rpt<T, 4, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-    default: return launch_flat_rpt<T, 8, VEC>(p, X, B, C, labels, scores, N, F, D, K, act, ws, stream);
-  }
+hipError_t launch_pack_small(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,
+                             void* out, hipStream_t stream) {
+  return dt == 0 ? pack_small_t<float>(B, C, F, D, K, out, stream)
+                 : pack_small_t<bf16raw>(B, C, F, D, K, out, stream);
 }
 
-hipError_t launch_small(const void* X, const void* B, const void* C, int32_t* labels,
+hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled, int32_t* labels,
                         float* scores, int64_t N, int64_t F, int64_t D, int64_t K, int dt,
                         int act, void* workspace, hipStream_t stream) {
-  SmallPlan p = plan_small(N, F, D, K, dt);
-  if (p.flat) {
-    const size_t align = dt == 0 ? 16 : 8;
-    const bool vec = (D % 4 == 0) && ((uintptr_t)B % align == 0);
-    const int n = (int)N, f = (int)F, d = (int)D, k = (int)K;
-    if (dt == 0)
-      return vec ? launch_flat_t<float, true>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
-                 : launch_flat_t<float, false>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
-    return vec ? launch_flat_t<bf16raw, true>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
-               : launch_flat_t<bf16raw, false>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
-  }
-  widen_for_final(p, N, K);
-  if (p.nb == 0) return hipErrorInvalidValue;
-  const int n = (int)N, f = (int)F, d = (int)D, k = (int)K;
-  if (p.mfma) {
-    switch (p.nb) {
-      case 1: return launch_mfma_ms<1>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
-      case 2: return launch_mfma_ms<2>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
-      case 3: return launch_mfma_ms<3>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
-      default: return launch_mfma_ms<4>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
-    }
-  }
   const size_t align = dt == 0 ? 16 : 8;
-  const bool vec = (D % 4 == 0) && ((uintptr_t)B % align == 0);
-  if (dt == 0)
-    return vec ? launch_valu_t<float, true>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
-               : launch_valu_t<float, false>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
-  return vec ? launch_valu_t<bf16raw, true>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream)
-             : launch_valu_t<bf16raw, false>(p, X, B, C, labels, scores, n, f, d, k, act, workspace, stream);
+  int lay = kTiled;
+  if (tiled) {
+    // the packed image's column-tiled section
+    const size_t es = dt == 0 ? 4 : 2;
+    C = static_cast<const char*>(B) + (cdiv(D, kW) * F * kW * es + 255) / 256 * 256;
+  } else {
+    const bool vec = (D % 4 == 0) && ((uintptr_t)B % align == 0) && ((uintptr_t)C % align == 0);
+    lay = vec ? kRawVec : kRawScalar;
+  }
+  SmallPlan p = plan_small(N, F, D, K, dt, lay, (uintptr_t)X % 16 == 0);
+  if (p.nb == 0) return hipErrorInvalidValue;
+  const Args a{X, B, C, labels, scores, (int)N, (int)F, (int)D, (int)K, act, workspace, stream};
+  return dt == 0 ? launch_t<float>(p, lay, a) : launch_t<bf16raw>(p, lay, a);
 }
 
 }  // namespace hd

@@ -45,7 +45,7 @@ def test_status_strings(L):
 def test_workspace_sizes(L):
     # small batch: 256-byte ticket header + replicated accumulators
     small = L.hd_infer_workspace_bytes(32, 561, 10240, 6, hd.HD_F32)
-    assert small == 256 + 4 * 32 * 32 * 6
+    assert small == 256 * 33 + 4 * 32 * 32 * 6  # counters, then 32 score replicas
     assert L.hd_infer_workspace_bytes(0, 561, 10240, 6, hd.HD_F32) == 0
     assert L.hd_infer_workspace_bytes(5, 0, 10, 6, hd.HD_F32) == 0
     # large batch, raw entry: holds the tiled model
