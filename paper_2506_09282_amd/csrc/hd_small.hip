@@ -64,7 +64,14 @@ __host__ __device__ inline SmallWs small_ws(void* ws) {
   return w;
 }
 
-__host__ __device__ inline int replicas(int G) { return G < kSmallReplicas ? G : kSmallReplicas; }
+// Score replicas: enough that few workgroups add into each address (atomics
+// on one address are serialised), few enough that the finishing workgroup
+// reads all of them in one batch (R*N*K <= 16 per thread).
+__host__ __device__ inline int replicas(int G, int NK) {
+  int r = (16 * 256) / (NK > 0 ? NK : 1);
+  r = r < 4 ? 4 : r > kSmallReplicas ? kSmallReplicas : r;
+  return G < r ? G : r;
+}
 
 // Block order. Workgroups are dispatched round-robin over the 8 XCDs, so
 // workgroup b runs on XCD b % 8. The blocks are split evenly between XCDs
@@ -394,7 +401,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
   const int cg = tid % kCG, rg = tid / kCG;
   const int G = gridDim.x;
   const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
-  const int R = replicas(G);
+  const int R = replicas(G, N * K);
   const int nmine = walk.count();
   const int nitems = nmine * nchunks;
 
@@ -537,7 +544,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = gridDim.x;
   const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
-  const int R = replicas(G);
+  const int R = replicas(G, N * K);
   const int nb = min(NB, N);
   const int npairs = nb * K;
   const int arow = wave * FQ + (lane >> 4);  // A-operand row of step 0
@@ -636,7 +643,7 @@ __global__ __launch_bounds__(kThreads) void small_flat_kernel(
   const int cg = tid % kCG, rg = tid / kCG;
   const int G = gridDim.x;
   const int blk = xcd_block(blockIdx.x, G);
-  const int R = replicas(G);
+  const int R = replicas(G, N * K);
   const int64_t d0 = (int64_t)blk * kW;
   const int npairs = N * K;
 
@@ -738,7 +745,7 @@ __global__ __launch_bounds__(kThreads) void small_block_mfma_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = gridDim.x;
   const int blk = xcd_block(blockIdx.x, G);
-  const int R = replicas(G);
+  const int R = replicas(G, N * K);
   const int nb = min(NB, N);
   const int npairs = nb * K;
   const int arow = wave * FQ + (lane >> 4);
@@ -833,6 +840,166 @@ __global__ __launch_bounds__(kThreads) void small_block_mfma_kernel(
   publish_and_finish(none, 0, 0, N, K, R, ws, labels, scores, smem, lds_floats, true);
 }
 
+// ---------------------------------------------------------------------------
+// Fragment matrix-core kernel (fp32, 8 < N <= 64, packed model). The packed
+// model holds, per 16-column block, the 16x16x4 A operands in the order the
+// waves consume them (see pack_frag_kernel): wave w's lane l = (d, q) with
+// d = l % 16, q = l / 16 covers the MS consecutive rows
+// f = 4*MS*w + MS*q + 0..MS-1 of column 16 blk + d, four rows per float4, so
+// a block costs each lane MS/4 16-byte loads and each wave-wide load is one
+// contiguous 1 KiB run. Matrix step s of the wave multiplies row
+// 4*MS*w + MS*q + s (lane group q) with the same rows of X^T, read from a
+// verbatim copy of X in LDS.
+//
+// Persistent: one workgroup per CU walks its column blocks with two blocks of
+// B in flight (ring3), X stays in LDS, and the workgroup's partial scores
+// accumulate in LDS and are published once.
+// LDS: sl[NB*K] | red[4][NTI][256] | hs[NB][17] | xs[NB*F + 16*MS] (+ 4 spare)
+// ---------------------------------------------------------------------------
+template <int MS>
+struct FragBuf {
+  float4 a[MS / 4];
+  float c[kW];
+};
+
+template <int NTI, int MS>
+__global__ __launch_bounds__(kThreads, 1) void small_frag_mfma_kernel(
+    const float* __restrict__ X, const float4* __restrict__ Bf, const float* __restrict__ C,
+    int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
+    int nblocks, int lds_floats, void* __restrict__ workspace) {
+  constexpr int NB = 16 * NTI;
+  constexpr int G4 = MS / 4;
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  float* sl = smem;                           // [NB*K]
+  float* red = sl + (NB * K + 3) / 4 * 4;     // [4][NTI][256]
+  float* hs = red + kWaves * NTI * 256;       // [NB][17]
+  float* xs = hs + (NB * (kW + 1) + 3) / 4 * 4;  // [NB*F + 16*MS] + 4 spare
+  const SmallWs ws = small_ws(workspace);
+  const ColView<float, kTiled> cv{C, D, K};
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int G = gridDim.x;
+  const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
+  const int R = replicas(G, N * K);
+  const int nb = min(NB, N);
+  const int npairs = nb * K;
+  const int nmine = walk.count();
+
+  auto load = [&](FragBuf<MS>& x, int i) {
+    const int blk = walk.block_of(i);
+    const float4* p = Bf + ((int64_t)blk * kWaves + wave) * G4 * kWave + lane;
+#pragma unroll
+    for (int g = 0; g < G4; ++g) x.a[g] = p[g * kWave];
+    load_c_pair(cv, K, blk, npairs, x.c);
+  };
+  // X is copied verbatim into LDS (xs[n*F + f]), before any B load is
+  // issued: a wait for a load also waits for every load issued before it,
+  // and X (shared by all workgroups, in L2) would otherwise wait for HBM.
+  // Each workgroup starts at a different offset so that they do not all read
+  // the same L2 lines at once. Stores are unconditional (past the end they go
+  // to the spare slot) so that no load is sunk to its store. Steps past F
+  // read the next row (finite values times zero B) or, after the last row,
+  // the zeroed run of 16*MS floats.
+  const int n4 = nb * F / 4;
+  {
+    const int rot = (int)(((int64_t)blockIdx.x * 37 * 64) % n4);
+    const float4* x4 = reinterpret_cast<const float4*>(X);
+    float4* xs4 = reinterpret_cast<float4*>(xs);
+    const int spare4 = (NB * F + 16 * MS + 3) / 4;
+    constexpr int kXB = NTI * MS / 4 < 40 ? NTI * MS / 4 : 40;
+    for (int base = 0; base < n4; base += kThreads * kXB) {
+      float4 v[kXB];
+      int at[kXB];
+#pragma unroll
+      for (int j = 0; j < kXB; ++j) {
+        const int i = base + j * kThreads + tid;
+        const int r = i + rot >= n4 ? i + rot - n4 : i + rot;
+        at[j] = i < n4 ? r : spare4;
+        v[j] = x4[i < n4 ? r : rot];
+      }
+#pragma unroll
+      for (int j = 0; j < kXB; ++j) xs4[at[j]] = v[j];
+    }
+    for (int e = 4 * n4 + tid; e < nb * F; e += kThreads) xs[e] = X[e];
+    for (int e = tid; e < 16 * MS; e += kThreads) xs[nb * F + e] = 0.0f;
+  }
+  // B for the first two blocks goes out once X is on chip
+  FragBuf<MS> b0, b1, b2;
+  ring3_start(nmine, b0, b1, load);
+  for (int p = tid; p < NB * K; p += kThreads) sl[p] = 0.0f;
+  __syncthreads();
+
+  const int xoff = (lane & 15) * F + 4 * MS * wave + MS * (lane >> 4);
+  auto process = [&](const FragBuf<MS>& x, int i) {
+    const int blk = walk.block_of(i);
+    const int64_t d0 = (int64_t)blk * kW;
+    // two independent accumulator chains per sample tile (steps 4g, 4g+2
+    // and 4g+1, 4g+3), interleaved over the tiles, so consecutive matrix
+    // instructions do not wait on each other's results
+    f32x4 acc[NTI][2];
+#pragma unroll
+    for (int t = 0; t < NTI; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int g = 0; g < G4; ++g) {
+      float4 xg[NTI];
+#pragma unroll
+      for (int t = 0; t < NTI; ++t) {
+        const float* q = xs + xoff + 16 * t * F + 4 * g;
+        xg[t] = make_float4(q[0], q[1], q[2], q[3]);
+      }
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].x, xg[t].x, acc[t][0], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].y, xg[t].y, acc[t][1], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].z, xg[t].z, acc[t][0], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].w, xg[t].w, acc[t][1], 0, 0, 0);
+    }
+    __syncthreads();  // previous block's readers of red / hs are done
+#pragma unroll
+    for (int t = 0; t < NTI; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        red[(wave * NTI + t) * 256 + (4 * (lane >> 4) + r) * 16 + (lane & 15)] =
+            acc[t][0][r] + acc[t][1][r];
+    __syncthreads();
+    for (int e = tid; e < NB * kW; e += kThreads) {
+      const int n = e / kW, c = e % kW;
+      const int t = n / 16, j = n % 16;
+      float v = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) v += red[(w * NTI + t) * 256 + c * 16 + j];
+      hs[n * (kW + 1) + c] = (d0 + c < D && n < nb) ? activate(v, act) : 0.0f;
+    }
+    __syncthreads();
+    block_scores(cv, hs, sl, npairs, K, blk, x.c);
+  };
+  ring3_run(nmine, b0, b1, b2, load, process);
+  __syncthreads();
+  publish_and_finish(sl, 0, nb, N, K, R, ws, labels, scores, smem, lds_floats, true);
+}
+
+// Writes the fragment section: out[((blk*4 + w)*(MS/4) + g)*64 + l][e] =
+// B[4*MS*w + MS*(l/16) + 4g + e][16 blk + l%16], zero past F or D.
+__global__ __launch_bounds__(256) void pack_frag_kernel(const float* __restrict__ B,
+                                                        float* __restrict__ out, int64_t F,
+                                                        int64_t D, int64_t nblk, int MS) {
+  const int64_t per_blk = (int64_t)256 * MS;  // 16 columns x 16*MS rows
+  const int64_t total = nblk * per_blk;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * 256) {
+    const int64_t e = i % 4, l = (i / 4) % 64, g = (i / 256) % (MS / 4),
+                  w = (i / (64 * MS)) % 4, blk = i / per_blk;
+    const int64_t f = 4 * MS * w + MS * (l / 16) + 4 * g + e;
+    const int64_t col = blk * kW + l % 16;
+    out[i] = (f < F && col < D) ? B[f * D + col] : 0.0f;
+  }
+}
+
 int num_cus() {
   static const int cus = [] {
     int dev = 0, v = 0;
@@ -851,6 +1018,7 @@ struct SmallPlan {
   bool flat;  // one block per workgroup (N <= 8)
   int rpt;    // flat kernel: rows per thread per chunk
   bool bmfma;  // block matrix-core kernel (one block per workgroup, N <= 32)
+  bool frag;   // fragment matrix-core kernel (packed model)
   bool mfma;
   int nb;    // VALU samples per pass, or MFMA sample tiles
   int ms;    // MFMA steps per wave
@@ -884,14 +1052,45 @@ SmallPlan plan_valu(int64_t N, int64_t F, int64_t D, int64_t K) {
   return p;
 }
 
-// Kernel choice: N <= 8 takes the flat kernel, fp32 with 8 < N <= 64 the
-// matrix-core kernel when its LDS fits; raw matrices with unaligned bases or
-// D % 4 != 0 (kRawScalar) and everything else take the VALU kernel.
+// Fragment section: rows per lane (MS) for F, or 0 when F is outside
+// [4, 16 * 64] (the section is then absent).
+constexpr int kFragMS[] = {12, 24, 36, 48, 64};
+int frag_ms(int64_t F) {
+  if (F < 4) return 0;
+  for (int ms : kFragMS)
+    if (16 * (int64_t)ms >= F) return ms;
+  return 0;
+}
+
+size_t frag_bytes(int64_t F, int64_t D, int dt) {
+  const int ms = dt == 0 ? frag_ms(F) : 0;
+  return (size_t)cdiv(D, kW) * 256 * ms * sizeof(float);
+}
+
+// Kernel choice: N <= 8 takes the flat kernel; fp32 with 8 < N <= 64 a
+// matrix-core kernel (the fragment kernel on a packed model, else the block
+// kernel for N <= 32 or the persistent one) when its LDS fits; raw matrices
+// with unaligned bases or D % 4 != 0 (kRawScalar) and everything else take
+// the VALU kernel.
 SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay, bool x_aligned) {
   SmallPlan v = plan_valu(N, F, D, K);
   if (v.nb == 0 || lay == kRawScalar) return v;
   SmallPlan p{};
   p.nblocks = v.nblocks;
+  if (lay == kTiled && dt == 0 && x_aligned && N > 8 && frag_ms(F) > 0) {
+    const int nti = (int)cdiv(N, 16), ms = frag_ms(F);
+    const int64_t nbk = 16 * nti;
+    const int64_t floats = (nbk * K + 3) / 4 * 4 + kWaves * nti * 256 +
+                           (nbk * (kW + 1) + 3) / 4 * 4 + (nbk * F + 16 * ms + 3) / 4 * 4 + 4;
+    if ((int64_t)sizeof(float) * floats <= kLdsBudget) {
+      p.frag = true;
+      p.nb = nti;
+      p.ms = ms;
+      p.lds = sizeof(float) * (size_t)floats;
+      p.grid = v.grid;
+      return p;
+    }
+  }
   if (N <= 8) {
     p.flat = true;
     p.nb = N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : 8;
@@ -940,7 +1139,7 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay
 // The last workgroup reuses all of LDS to sum the R score replicas, so give
 // the launch at least R*N*K floats when that fits.
 void widen_for_final(SmallPlan& p, int64_t N, int64_t K) {
-  const size_t want = sizeof(float) * (size_t)replicas(p.grid) * N * K;
+  const size_t want = sizeof(float) * (size_t)replicas(p.grid, (int)(N * K)) * N * K;
   if (p.lds < want && want <= (size_t)kLdsBudget) p.lds = want;
 }
 
@@ -1020,6 +1219,37 @@ hipError_t launch_bmfma_ms(const SmallPlan& p, const Args& a) {
     case 24: return launch_bmfma<NTI, 24, LAY>(p, a);
     case 36: return launch_bmfma<NTI, 36, LAY>(p, a);
     default: return launch_bmfma<NTI, 48, LAY>(p, a);
+  }
+}
+
+template <int NTI, int MS>
+hipError_t launch_frag(const SmallPlan& p, const Args& a, const void* frag) {
+  static const hipError_t attr = allow_lds(&small_frag_mfma_kernel<NTI, MS>);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((small_frag_mfma_kernel<NTI, MS>), dim3(p.grid), dim3(kThreads), p.lds,
+                     a.stream, (const float*)a.X, (const float4*)frag, (const float*)a.C,
+                     a.labels, a.scores, a.N, a.F, a.D, a.K, a.act, p.nblocks,
+                     (int)(p.lds / sizeof(float)), a.ws);
+  return hipGetLastError();
+}
+
+template <int NTI>
+hipError_t launch_frag_ms(const SmallPlan& p, const Args& a, const void* frag) {
+  switch (p.ms) {
+    case 12: return launch_frag<NTI, 12>(p, a, frag);
+    case 24: return launch_frag<NTI, 24>(p, a, frag);
+    case 36: return launch_frag<NTI, 36>(p, a, frag);
+    case 48: return launch_frag<NTI, 48>(p, a, frag);
+    default: return launch_frag<NTI, 64>(p, a, frag);
+  }
+}
+
+hipError_t launch_frag_nti(const SmallPlan& p, const Args& a, const void* frag) {
+  switch (p.nb) {
+    case 1: return launch_frag_ms<1>(p, a, frag);
+    case 2: return launch_frag_ms<2>(p, a, frag);
+    case 3: return launch_frag_ms<3>(p, a, frag);
+    default: return launch_frag_ms<4>(p, a, frag);
   }
 }
 
@@ -1131,20 +1361,37 @@ size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt)
 const char* small_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   const SmallPlan p = plan_small(N, F, D, K, dt, tiled ? kTiled : kRawVec, true);
   if (p.nb == 0) return "";
-  return p.flat ? "small_flat_kernel" : p.bmfma ? "small_block_mfma_kernel"
+  return p.flat ? "small_flat_kernel" : p.frag ? "small_frag_mfma_kernel"
+                                      : p.bmfma ? "small_block_mfma_kernel"
                                       : p.mfma  ? "small_mfma_kernel" : "small_valu_kernel";
 }
 
-size_t small_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {
+// Small-batch section of a packed model: column tiles of B, column tiles of
+// C, then (fp32, 4 <= F <= 1024) the fragment copy of B, each on a 256-byte
+// boundary.
+size_t small_tiles_bytes(int64_t F, int64_t D, int64_t K, int dt) {
   const size_t es = dt == 0 ? 4 : 2;
   const size_t nblk = (size_t)cdiv(D, kW);
   return (nblk * F * kW * es + 255) / 256 * 256 + (nblk * K * kW * es + 255) / 256 * 256;
 }
 
+size_t small_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {
+  return small_tiles_bytes(F, D, K, dt) + (frag_bytes(F, D, dt) + 255) / 256 * 256;
+}
+
 hipError_t launch_pack_small(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,
                              void* out, hipStream_t stream) {
-  return dt == 0 ? pack_small_t<float>(B, C, F, D, K, out, stream)
-                 : pack_small_t<bf16raw>(B, C, F, D, K, out, stream);
+  const hipError_t e = dt == 0 ? pack_small_t<float>(B, C, F, D, K, out, stream)
+                               : pack_small_t<bf16raw>(B, C, F, D, K, out, stream);
+  if (e != hipSuccess || frag_bytes(F, D, dt) == 0) return e;
+  const int64_t nblk = cdiv(D, kW);
+  const int ms = frag_ms(F);
+  const int64_t g = cdiv(nblk * 256 * ms, 256);
+  hipLaunchKernelGGL(pack_frag_kernel, dim3((unsigned)(g < 65536 ? g : 65536)), dim3(256), 0,
+                     stream, (const float*)B,
+                     reinterpret_cast<float*>(static_cast<char*>(out) + small_tiles_bytes(F, D, K, dt)),
+                     F, D, nblk, ms);
+  return hipGetLastError();
 }
 
 hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled, int32_t* labels,
@@ -1152,10 +1399,12 @@ hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled,
                         int act, void* workspace, hipStream_t stream) {
   const size_t align = dt == 0 ? 16 : 8;
   int lay = kTiled;
+  const void* frag = nullptr;
   if (tiled) {
-    // the packed image's column-tiled section
+    // the packed image's small-batch section
     const size_t es = dt == 0 ? 4 : 2;
     C = static_cast<const char*>(B) + (cdiv(D, kW) * F * kW * es + 255) / 256 * 256;
+    if (frag_bytes(F, D, dt) > 0) frag = static_cast<const char*>(B) + small_tiles_bytes(F, D, K, dt);
   } else {
     const bool vec = (D % 4 == 0) && ((uintptr_t)B % align == 0) && ((uintptr_t)C % align == 0);
     lay = vec ? kRawVec : kRawScalar;
@@ -1163,6 +1412,11 @@ hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled,
   SmallPlan p = plan_small(N, F, D, K, dt, lay, (uintptr_t)X % 16 == 0);
   if (p.nb == 0) return hipErrorInvalidValue;
   const Args a{X, B, C, labels, scores, (int)N, (int)F, (int)D, (int)K, act, workspace, stream};
+  if (p.frag) {
+    if (!frag) return hipErrorInvalidValue;
+    widen_for_final(p, N, K);
+    return launch_frag_nti(p, a, frag);
+  }
   return dt == 0 ? launch_t<float>(p, lay, a) : launch_t<bf16raw>(p, lay, a);
 }
 

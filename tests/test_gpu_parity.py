@@ -189,14 +189,17 @@ def test_packed_model_matches_raw(hd, N, dtype):
         assert np.all(np.abs(S0 - S1) <= 1e-6 * c1[None, :])
 
 
-# Packed model on the small-batch path: the column-tiled section (zero past
-# column D) against the oracle, covering every small kernel: the flat kernel
-# (N <= 8, one and several f-chunks), the matrix-core kernel (fp32, N > 8) and
-# the VALU kernel (bf16, N > 8).
+# Packed model on the small-batch path against the oracle, covering every
+# small kernel: the flat kernel on the column tiles (N <= 8, one and several
+# f-chunks), the fragment matrix-core kernel (fp32, N > 8: one to four sample
+# tiles, every rows-per-lane size, rows that wrap inside a float4 of X), the
+# persistent matrix-core kernel where the fragment kernel's LDS does not fit,
+# and the VALU kernel (bf16, N > 8).
 PACKED_SMALL = [(1, 561, 10240, 6, "f32"), (3, 20, 1000, 4, "f32"), (8, 1100, 777, 9, "f32"),
                 (7, 300, 2050, 3, "bf16"), (9, 64, 1000, 5, "f32"), (32, 561, 10240, 6, "f32"),
                 (64, 561, 4096, 6, "f32"), (40, 130, 3000, 100, "f32"), (20, 90, 1000, 7, "bf16"),
-                (64, 1500, 513, 3, "bf16"), (17, 900, 333, 2, "f32")]
+                (64, 1500, 513, 3, "bf16"), (17, 900, 333, 2, "f32"), (64, 200, 1000, 3, "f32"),
+                (12, 5, 64, 3, "f32"), (16, 4, 100, 2, "f32"), (48, 700, 2000, 26, "f32")]
 
 
 @pytest.mark.parametrize("N,F,D,K,dtype", PACKED_SMALL)
