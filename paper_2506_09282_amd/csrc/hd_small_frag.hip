@@ -1,0 +1,315 @@
+// Small-batch matrix-core kernel on the packed fragment layout.
+#include "hd_small.hpp"
+
+namespace hd {
+namespace sp {
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Fragment matrix-core kernel (fp32, 8 < N <= 64, packed model). The packed
+// model holds, per 16-column block, the 16x16x4 A operands in the order the
+// waves consume them (see pack_frag_kernel): compute wave w's lane
+// l = (d, q), d = l % 16, q = l / 16, covers the MS consecutive rows
+// f = 4*MS*w + MS*q + 0..MS-1 of column 16 blk + d, four rows per float4, so
+// a block costs each lane MS/4 16-byte loads and each wave-wide load is one
+// contiguous 1 KiB run. Matrix step s of the wave multiplies row
+// 4*MS*w + MS*q + s (lane group q) with the same rows of X^T, read from a
+// verbatim copy of X in LDS.
+//
+// Persistent, one 512-thread workgroup per CU walking its column blocks,
+// with the waves split by role so that memory, matrix and reduction work
+// overlap:
+//   waves 4..7 (compute): hold three blocks of B in flight and run the
+//     matrix instructions of block i, leaving their partial V (each over a
+//     quarter of F) in red[i % 2];
+//   waves 0..3 (finish): first stage X and the C values of every block of
+//     the workgroup into LDS (their loads do not queue behind B, since load
+//     counters are per wave), then, while block i is multiplied, turn block
+//     i-1's partials into HardSign values and per-pair partial scores
+//     (Eq. 1, Eq. 8).
+// One barrier per block hands red from one role to the other.
+// LDS: sl[NB*K] | red[2][4 waves][NTI][16 n][16 d] | cs[cslots][K*16] |
+//      xs[NB*F + 16*MS] (+ 4 spare), cslots >= blocks per workgroup
+// ---------------------------------------------------------------------------
+
+template <int MS>
+struct FragBuf {
+  float4 a[MS / 4];
+};
+
+template <int NTI, int MS>
+__global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
+    const float* __restrict__ X, const float4* __restrict__ Bf, const float* __restrict__ C,
+    int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
+    int nblocks, int cslots, int lds_floats, void* __restrict__ workspace) {
+  constexpr int NB = 16 * NTI;
+  constexpr int G4 = MS / 4;
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  float* sl = smem;                          // [NB*K]
+  float* red = sl + (NB * K + 3) / 4 * 4;    // [2][4][NTI][16][16]
+  float* cs = red + 2 * kWaves * NTI * 256;  // [cslots][K*16]: C of block i at slot i
+  float* xs = cs + cslots * K * kW;          // [NB*F + 16*MS] + 4 spare
+  const SmallWs ws = small_ws(workspace);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const bool compute = wave >= kWaves;
+  const int cw = wave - kWaves;  // compute wave index
+  const int G = gridDim.x;
+  const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
+  const int R = replicas(G, N * K);
+  const int nb = min(NB, N);
+  const int npairs = nb * K;
+  const int nmine = walk.count();
+
+  // compute waves: B fragments of blocks 0, 1, 2
+  FragBuf<MS> b0, b1, b2;
+  // Blocks past the workgroup's last one are "loaded" from a single
+  // broadcast address (one 16-byte request per wave instruction), so the
+  // load count per step never depends on a branch.
+  auto load_b = [&](FragBuf<MS>& x, int i) {
+    const float4* p = i < nmine
+        ? Bf + ((int64_t)walk.block_of(i) * kWaves + cw) * G4 * kWave + lane : Bf;
+    const int stride = i < nmine ? kWave : 0;
+#pragma unroll
+    for (int g = 0; g < G4; ++g) x.a[g] = p[g * stride];
+  };
+
+  if (compute) {  // the third block goes out after the barrier
+    load_b(b0, 0);
+    load_b(b1, 1);
+  } else {
+    // X copied verbatim into LDS (xs[n*F + f]). Each workgroup starts at a
+    // different offset so that they do not all read the same L2 lines at
+    // once; stores are unconditional (past the end they go to the spare
+    // slot) so that no load is sunk to its store. Steps past F read the next
+    // row (finite values times zero B) or, after the last row, the zeroed
+    // run of 16*MS floats.
+    const int n4 = nb * F / 4;
+    const int rot = (int)(((int64_t)blockIdx.x * 37 * 64) % n4);
+    const float4* x4 = reinterpret_cast<const float4*>(X);
+    float4* xs4 = reinterpret_cast<float4*>(xs);
+    const int spare4 = (NB * F + 16 * MS + 3) / 4;
+    constexpr int kXB = NTI * MS / 4 < 40 ? NTI * MS / 4 : 40;
+    for (int base = 0; base < n4; base += kThreads * kXB) {
+      float4 v[kXB];
+      int at[kXB];
+#pragma unroll
+      for (int j = 0; j < kXB; ++j) {
+        const int i = base + j * kThreads + tid;
+        const int r = i + rot >= n4 ? i + rot - n4 : i + rot;
+        at[j] = i < n4 ? r : spare4;
+        v[j] = x4[i < n4 ? r : rot];
+      }
+#pragma unroll
+      for (int j = 0; j < kXB; ++j) xs4[at[j]] = v[j];
+    }
+    for (int e = 4 * n4 + tid; e < nb * F; e += kThreads) xs[e] = X[e];
+    for (int e = tid; e < 16 * MS; e += kThreads) xs[nb * F + e] = 0.0f;
+    // block i's K*16 C values are one contiguous run of the column tiles
+    const int kc4 = K * kW / 4;
+    for (int e = tid; e < nmine * kc4; e += kThreads) {
+      const int b = e / kc4, r = e - b * kc4;
+      reinterpret_cast<float4*>(cs)[e] =
+          reinterpret_cast<const float4*>(C + (int64_t)walk.block_of(b) * K * kW)[r];
+    }
+  }
+  __syncthreads();
+
+  // X operands of the compute waves: they do not depend on the block, so
+  // when the registers allow they are read from LDS once into registers
+  // (no LDS latency between matrix instructions)
+  constexpr bool kXReg = 3 * MS + NTI * MS <= 180;
+  const int xoff = (lane & 15) * F + 4 * MS * cw + MS * (lane >> 4);
+  float4 xr[kXReg ? G4 : 1][kXReg ? NTI : 1];
+  if (compute) {
+    if (kXReg) {
+#pragma unroll
+      for (int g = 0; g < (kXReg ? G4 : 1); ++g)
+#pragma unroll
+        for (int t = 0; t < (kXReg ? NTI : 1); ++t) {
+          const float* q = xs + xoff + 16 * t * F + 4 * g;
+          xr[g][t] = make_float4(q[0], q[1], q[2], q[3]);
+        }
+    }
+    load_b(b2, 2);
+  }
+  auto multiply = [&](const FragBuf<MS>& x, int i) {
+    // two independent accumulator chains per sample tile (steps 4g, 4g+2
+    // and 4g+1, 4g+3), interleaved over the tiles
+    f32x4 acc[NTI][2];
+#pragma unroll
+    for (int t = 0; t < NTI; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int g = 0; g < G4; ++g) {
+      float4 xg[NTI];
+#pragma unroll
+      for (int t = 0; t < NTI; ++t) {
+        if constexpr (kXReg) {
+          xg[t] = xr[g][t];
+        } else {
+          const float* q = xs + xoff + 16 * t * F + 4 * g;
+          xg[t] = make_float4(q[0], q[1], q[2], q[3]);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].x, xg[t].x, acc[t][0], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].y, xg[t].y, acc[t][1], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].z, xg[t].z, acc[t][0], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].w, xg[t].w, acc[t][1], 0, 0, 0);
+    }
+    // lane l holds V^T[d = 4(l/16) + q][n = l%16], q = 0..3: one 16-byte
+    // store into red[i % 2][cw][t][n][d]
+    float4* r = reinterpret_cast<float4*>(red + ((i & 1) * kWaves + cw) * NTI * 256) +
+                (lane & 15) * 4 + (lane >> 4);
+#pragma unroll
+    for (int t = 0; t < NTI; ++t)
+      r[t * 64] = make_float4(acc[t][0][0] + acc[t][1][0], acc[t][0][1] + acc[t][1][1],
+                              acc[t][0][2] + acc[t][1][2], acc[t][0][3] + acc[t][1][3]);
+  };
+  // Block i's partial scores. Finish thread (n, g), a quad of lanes per
+  // sample n, sums the four wave partials of V[n][4g .. 4g+3], applies
+  // HardSign, and forms its 4-term share of every class's inner product
+  // (K <= kFragMaxK, all C reads issued at once); the quad adds its shares
+  // with DPP and lane g keeps classes k = g mod 4 in registers across blocks.
+  // Columns past D need no mask: the packed C is zero there.
+  const int fn = tid >> 2, fg = tid & 3;
+  float sacc[kFragMaxK / 4];
+#pragma unroll
+  for (int j = 0; j < kFragMaxK / 4; ++j) sacc[j] = 0.0f;
+  auto finish = [&](int i) {
+    if (fn >= nb) return;  // whole quads drop out together
+    const float4* r4 = reinterpret_cast<const float4*>(red + (i & 1) * kWaves * NTI * 256);
+    const float4* c4 = reinterpret_cast<const float4*>(cs + i * K * kW);
+    float4 c[kFragMaxK];
+#pragma unroll
+    for (int k = 0; k < kFragMaxK; ++k) c[k] = c4[(k < K ? k : 0) * 4 + fg];
+    float4 v = r4[fn * 4 + fg];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) {
+      const float4 u = r4[w * NTI * 64 + fn * 4 + fg];
+      v.x += u.x;
+      v.y += u.y;
+      v.z += u.z;
+      v.w += u.w;
+    }
+    const float h0 = activate(v.x, act), h1 = activate(v.y, act), h2 = activate(v.z, act),
+                h3 = activate(v.w, act);
+#pragma unroll
+    for (int k = 0; k < kFragMaxK; ++k) {
+      float d = fmaf(h0, c[k].x, fmaf(h1, c[k].y, fmaf(h2, c[k].z, h3 * c[k].w)));
+      d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                         0, __builtin_bit_cast(int, d), 0xB1, 0xf, 0xf, false));
+      d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                         0, __builtin_bit_cast(int, d), 0x4E, 0xf, 0xf, false));
+      sacc[k >> 2] += (k & 3) == fg ? d : 0.0f;
+    }
+  };
+  // Step i (one barrier each, nmine + 1 steps): compute waves multiply block
+  // i and reload its buffer with block i+3; finish waves finish block i-1.
+  // The two roles run separate loops with the same barrier count, so that
+  // the compiler's load-counter bookkeeping for the B ring never crosses the
+  // other role's code. B buffers are named per step (no register copies,
+  // which would wait on the loads).
+  if (compute) {
+    auto stepc = [&](FragBuf<MS>& b, int i) {
+      multiply(b, i);
+      load_b(b, i + 3);
+      __syncthreads();
+    };
+    for (int it = 0; it < nmine; it += 3) {
+      stepc(b0, it);
+      if (it + 1 >= nmine) break;
+      stepc(b1, it + 1);
+      if (it + 2 >= nmine) break;
+      stepc(b2, it + 2);
+    }
+    __syncthreads();  // the finish waves' last step
+  } else {
+    for (int i = 0; i <= nmine; ++i) {
+      if (i > 0) finish(i - 1);
+      __syncthreads();
+    }
+    if (fn < nb) {
+#pragma unroll
+      for (int k = 0; k < kFragMaxK; ++k)
+        if (k < K && (k & 3) == fg) sl[fn * K + k] = sacc[k >> 2];
+    }
+  }
+  __syncthreads();
+  publish_and_finish<kFragThreads>(sl, 0, nb, N, K, R, ws, labels, scores, smem, lds_floats,
+                                   true);
+}
+
+// Writes the fragment section: out[((blk*4 + w)*(MS/4) + g)*64 + l][e] =
+// B[4*MS*w + MS*(l/16) + 4g + e][16 blk + l%16], zero past F or D.
+__global__ __launch_bounds__(256) void pack_frag_kernel(const float* __restrict__ B,
+                                                        float* __restrict__ out, int64_t F,
+                                                        int64_t D, int64_t nblk, int MS) {
+  const int64_t per_blk = (int64_t)256 * MS;  // 16 columns x 16*MS rows
+  const int64_t total = nblk * per_blk;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * 256) {
+    const int64_t e = i % 4, l = (i / 4) % 64, g = (i / 256) % (MS / 4),
+                  w = (i / (64 * MS)) % 4, blk = i / per_blk;
+    const int64_t f = 4 * MS * w + MS * (l / 16) + 4 * g + e;
+    const int64_t col = blk * kW + l % 16;
+    out[i] = (f < F && col < D) ? B[f * D + col] : 0.0f;
+  }
+}
+
+
+template <int NTI, int MS>
+hipError_t launch_frag(const SmallPlan& p, const Args& a, const void* frag) {
+  static const hipError_t attr = allow_lds(&small_frag_mfma_kernel<NTI, MS>);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((small_frag_mfma_kernel<NTI, MS>), dim3(p.grid), dim3(kFragThreads), p.lds,
+                     a.stream, (const float*)a.X, (const float4*)frag, (const float*)a.C,
+                     a.labels, a.scores, a.N, a.F, a.D, a.K, a.act, p.nblocks, p.cslots,
+                     (int)(p.lds / sizeof(float)), a.ws);
+  return hipGetLastError();
+}
+
+template <int NTI>
+hipError_t launch_frag_ms(const SmallPlan& p, const Args& a, const void* frag) {
+  switch (p.ms) {
+    case 12: return launch_frag<NTI, 12>(p, a, frag);
+    case 24: return launch_frag<NTI, 24>(p, a, frag);
+    case 36: return launch_frag<NTI, 36>(p, a, frag);
+    case 48: return launch_frag<NTI, 48>(p, a, frag);
+    default: return launch_frag<NTI, 64>(p, a, frag);
+  }
+}
+
+hipError_t launch_frag_nti(const SmallPlan& p, const Args& a, const void* frag) {
+  switch (p.nb) {
+    case 1: return launch_frag_ms<1>(p, a, frag);
+    case 2: return launch_frag_ms<2>(p, a, frag);
+    case 3: return launch_frag_ms<3>(p, a, frag);
+    default: return launch_frag_ms<4>(p, a, frag);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_frag_family(SmallPlan& p, const Args& a, const void* frag) {
+  widen_for_final(p, a.N, a.K);
+  return launch_frag_nti(p, a, frag);
+}
+
+hipError_t launch_pack_frag(const void* B, void* out, int64_t F, int64_t D, int64_t nblk, int ms,
+                            hipStream_t stream) {
+  const int64_t g = cdiv(nblk * 256 * ms, 256);
+  hipLaunchKernelGGL(pack_frag_kernel, dim3((unsigned)(g < 65536 ? g : 65536)), dim3(256), 0,
+                     stream, (const float*)B, static_cast<float*>(out), F, D, nblk, ms);
+  return hipGetLastError();
+}
+
+}  // namespace sp
+}  // namespace hd

@@ -199,7 +199,8 @@ PACKED_SMALL = [(1, 561, 10240, 6, "f32"), (3, 20, 1000, 4, "f32"), (8, 1100, 77
                 (7, 300, 2050, 3, "bf16"), (9, 64, 1000, 5, "f32"), (32, 561, 10240, 6, "f32"),
                 (64, 561, 4096, 6, "f32"), (40, 130, 3000, 100, "f32"), (20, 90, 1000, 7, "bf16"),
                 (64, 1500, 513, 3, "bf16"), (17, 900, 333, 2, "f32"), (64, 200, 1000, 3, "f32"),
-                (12, 5, 64, 3, "f32"), (16, 4, 100, 2, "f32"), (48, 700, 2000, 26, "f32")]
+                (12, 5, 64, 3, "f32"), (16, 4, 100, 2, "f32"), (48, 700, 2000, 26, "f32"),
+                (24, 300, 1000, 16, "f32"), (10, 100, 500, 13, "f32")]
 
 
 @pytest.mark.parametrize("N,F,D,K,dtype", PACKED_SMALL)
