@@ -34,7 +34,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kPrefetch = 4;  // f-steps of B fragments in flight per wave
+constexpr int kPrefetchMin = 4;  // f-steps of B fragments in flight per wave
 constexpr int kMaxSlices = 16;  // D slices per sample tile (split-D)
 constexpr int kLdsBytes = 160 * 1024 - 256;  // leave room for static LDS
 
@@ -344,6 +344,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     int N, int F, int K, int ndb, int DS, int act, void* __restrict__ workspace) {
   typedef typename Tr::elem T;
   constexpr int NT = 32 * NTILES;
+  constexpr int kPrefetch = kPrefetchMin;
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   __shared__ int s_last;
 
@@ -361,7 +362,10 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
   const int u_end = (int)((int64_t)units * (slice + 1) / DS);
 
   // ---- X tile -> LDS (rows n0..n0+NT, zero padded) -------------------------
+  // A 16-byte zero slot follows the tile: padding f-steps past nfs read it.
   T* xt = reinterpret_cast<T*>(lds);
+  const T* xzero = xt + NT * pitch;
+  if (tid == 0) *reinterpret_cast<uint4*>(xt + NT * pitch) = make_uint4(0u, 0u, 0u, 0u);
   {
     // zero the padding columns F..nfs*kFStep and whole rows past N
     const int fpad = nfs * Tr::kFStep;
@@ -448,16 +452,22 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
 
   int u = u_begin + wave;
   uint4 afr[kPrefetch][2];
+  // B fragments through a buffer resource: 32-bit byte offsets, no 64-bit
+  // address arithmetic per load (the packed B is below 2 GiB)
+  const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(Bp), 0, ndb * nfs * 1024, 0x00020000);
   auto bfrag = [&](int uu, int fs, int b) -> uint4 {
-    return Bp[((int64_t)(2 * uu + b) * nfs + fs) * 64 + lane];
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         brsrc, ((2 * uu + b) * nfs + fs) * 1024 + lane * 16, 0, 0));
   };
   if (u < u_end) {
+    // slots past nfs hold a valid fragment too: padding steps multiply them
+    // by the zero slot, so they must be finite
 #pragma unroll
-    for (int i = 0; i < kPrefetch; ++i)
-      if (i < nfs) {
-        afr[i][0] = bfrag(u, i, 0);
-        afr[i][1] = bfrag(u, i, 1);
-      }
+    for (int i = 0; i < kPrefetch; ++i) {
+      afr[i][0] = bfrag(u, i < nfs ? i : nfs - 1, 0);
+      afr[i][1] = bfrag(u, i < nfs ? i : nfs - 1, 1);
+    }
   }
   for (; u < u_end; u += kWaves) {
     const int un = u + kWaves;
@@ -477,24 +487,25 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     for (int t = 0; t < NTILES; ++t)
       xfr[0][t] = *reinterpret_cast<const uint4*>(xlane + t * 32 * pitch);
 
-    // Every step issues the same loads unconditionally (addresses clamped to
-    // valid fragments) so the hardware wait counters can be tracked across
-    // the loop; only the memory-free MFMA block is predicated.
+    // Every step issues the same loads and matrix instructions
+    // unconditionally, with no branch in the loop body, so the compiler can
+    // interleave the refill arithmetic with the matrix instructions and track
+    // the wait counters across the loop. Padding steps past nfs (up to
+    // kPrefetch-1 of them) multiply a valid, finite B fragment by the zero
+    // slot.
     for (int fs0 = 0; fs0 < nfsl; fs0 += kPrefetch) {
 #pragma unroll
       for (int i = 0; i < kPrefetch; ++i) {
         const int fs = fs0 + i;
-        const int fsn = min(fs + 1, nfs - 1);
+        const int fsn = fs + 1;
 #pragma unroll
         for (int t = 0; t < NTILES; ++t)
-          xfr[(i + 1) & 1][t] =
-              *reinterpret_cast<const uint4*>(xlane + t * 32 * pitch + fsn * Tr::kFStep);
-        if (fs < nfs) {
+          xfr[(i + 1) & 1][t] = *reinterpret_cast<const uint4*>(
+              fsn < nfs ? xlane + t * 32 * pitch + fsn * Tr::kFStep : xzero);
 #pragma unroll
-          for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-            for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
-        }
+          for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
         // ring refill: step fs + kPrefetch of this unit, else the first steps
         // of the wave's next unit, else a harmless reload of a valid fragment
         const int nx = fs + kPrefetch;
@@ -608,11 +619,13 @@ template <class Tr>
 LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
   LargeCfg c{};
   if (cdiv(K, 32) > 4 || F > (1 << 20) || N > (1 << 30)) return c;
+  // B fragments are addressed with 32-bit byte offsets
+  if (cdiv(D, 64) * 2 * nfs_of<Tr>((int)F) * 1024 >= ((int64_t)1 << 31)) return c;
   const int pitch = pitch_of<Tr>((int)F);
   const int kbr = kb_of(K);
   for (int nt : {4, 2, 1}) {
     if (nt == 4 && kbr > 2) continue;
-    const size_t xbytes = (size_t)32 * nt * pitch * Tr::kEsz;
+    const size_t xbytes = (size_t)32 * nt * pitch * Tr::kEsz + 16;  // + zero slot
     const size_t rbytes = (size_t)kWaves * 32 * nt * 32 * kbr * 4;
     const size_t need = xbytes > rbytes ? xbytes : rbytes;
     if (need <= (size_t)kLdsBytes) {
