@@ -56,6 +56,7 @@ struct TrBF16 {
   static constexpr int kFStep = 16;
   static constexpr int kVec = 8;  // elements per 16-byte group
   static constexpr int kEsz = 2;
+  static constexpr int kStage1Mfma = 1;  // matrix instructions per stage1 call
   static constexpr int kCFrags = 2;  // 1 KiB C fragments per (d-block, class block)
   // LDS position of feature column c inside a sample row.
   __device__ static int lds_pos(int c) { return c; }
@@ -70,6 +71,7 @@ struct TrF32 {
   static constexpr int kFStep = 8;
   static constexpr int kVec = 4;
   static constexpr int kEsz = 4;
+  static constexpr int kStage1Mfma = 4;
   static constexpr int kCFrags = 4;
   // Within each group of 8 features the even ones are stored first, so a
   // lane of MFMA k-half g reads its four features (g, g+2, g+4, g+6) as one
@@ -506,6 +508,12 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
         for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
+        // instruction order per step: the next step's X reads (LDS) first, so
+        // they complete under this step's matrix instructions, then the
+        // matrix instructions, then the ring refill loads
+        __builtin_amdgcn_sched_group_barrier(0x100, NTILES, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES * Tr::kStage1Mfma, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
         // ring refill: step fs + kPrefetch of this unit, else the first steps
         // of the wave's next unit, else a harmless reload of a valid fragment
         const int nx = fs + kPrefetch;
