@@ -164,7 +164,7 @@ hd_status hd_infer(const void* X, const void* B, const void* C, int32_t* labels,
 const char* hd_infer_kernel(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, int packed) {
   if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return "";
   if (use_small(N, F, D, K, dt)) return hd::small_kernel_name(N, F, D, K, dt, packed != 0);
-  return hd::large_supported(N, F, D, K, dt) ? "large_fused_kernel" : "";
+  return hd::large_kernel_name(N, F, D, K, dt);
 }
 
 hd_status hd_infer_packed(const void* X, const void* packed, int32_t* labels, float* scores,

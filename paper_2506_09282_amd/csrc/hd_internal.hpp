@@ -35,6 +35,8 @@ hipError_t launch_similarity(const float* H, const void* C, int32_t* labels, flo
 
 // Large-batch fused path (MFMA, packed model).
 bool large_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
+// Name of the kernel launch_large uses for these sizes ("" if unsupported).
+const char* large_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 size_t large_packed_bytes(int64_t F, int64_t D, int64_t K, int dt);
 size_t large_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 hipError_t launch_pack(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,

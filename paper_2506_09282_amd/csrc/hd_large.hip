@@ -122,6 +122,13 @@ inline int kb_of(int64_t K) {
   return kb == 3 ? 4 : kb;
 }
 
+// Sample tiles per workgroup of the F-chunked kernel: 4 when the accumulators
+// fit in registers, fewer as class blocks grow.
+template <class Tr>
+constexpr int chunk_ntiles(int kb) {
+  return kb > 2 ? 1 : (kb == 2 && Tr::kEsz == 4) ? 2 : 4;
+}
+
 template <class Tr>
 PackGeom pack_geom(int64_t F, int64_t D, int64_t K) {
   PackGeom g;
@@ -336,6 +343,94 @@ __host__ __device__ inline LargeWs large_ws(void* ws, int64_t ntiles) {
   return w;
 }
 
+// Combine the waves' partial scores through LDS, then argmax (Eq. 9) and
+// write; with a split of D, publish this slice's partial scores and let the
+// tile's last slice finish (fixed slice order, so results are deterministic).
+template <int NTILES, int KB>
+__device__ void finish_tile(f32x16 (&sacc)[NTILES][KB], unsigned char* lds, int* s_last_p,
+                            int32_t* __restrict__ labels, float* __restrict__ scores, int N, int K,
+                            int DS, int ntiles, int slice, int tile, int n0,
+                            void* __restrict__ workspace) {
+  constexpr int NT = 32 * NTILES;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int& s_last = *s_last_p;
+  __syncthreads();  // X tile no longer needed
+  float* sred = reinterpret_cast<float*>(lds);  // [kWaves][NT][32*KB]
+  constexpr int KP = 32 * KB;
+#pragma unroll
+  for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int k = 32 * kb + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int n = 32 * t + (lane & 31);
+        sred[((int64_t)wave * NT + n) * KP + k] = sacc[t][kb][r];
+      }
+  __syncthreads();
+  const int rows = min(NT, N - n0);
+  if (DS == 1) {
+    for (int n = tid; n < rows; n += kThreads) {
+      float best = 0.0f;
+      int best_k = 0;
+      for (int k = 0; k < K; ++k) {
+        float s = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) s += sred[((int64_t)w * NT + n) * KP + k];
+        if (scores) scores[(int64_t)(n0 + n) * K + k] = s;
+        if (k == 0 || s > best) {
+          best = s;
+          best_k = k;
+        }
+      }
+      labels[n0 + n] = best_k;
+    }
+    return;
+  }
+  // Split-D: publish this slice's partial, the last slice of the tile finishes
+  // (summing the slices in a fixed order, so results are deterministic).
+  const LargeWs ws = large_ws(workspace, ntiles);
+  float* mypart = ws.part + (int64_t)slice * N * K;
+  for (int i = tid; i < rows * K; i += kThreads) {
+    const int n = i / K, k = i - n * K;
+    float s = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += sred[((int64_t)w * NT + n) * KP + k];
+    publish_store(mypart + (int64_t)(n0 + n) * K + k, s);
+  }
+  wait_own_memory_ops();
+  __syncthreads();
+  if (tid == 0) s_last = (take_ticket(ws.counters + tile) == (unsigned)DS - 1) ? 1 : 0;
+  __syncthreads();
+  if (!s_last) return;
+  for (int i = tid; i < rows * K; i += kThreads) {
+    const int n = i / K, k = i - n * K;
+    float t[kMaxSlices];
+#pragma unroll
+    for (int sl = 0; sl < kMaxSlices; ++sl)
+      t[sl] = sl < DS ? take_and_clear(ws.part + ((int64_t)sl * N + n0 + n) * K + k) : 0.0f;
+    float s = 0.0f;
+#pragma unroll
+    for (int sl = 0; sl < kMaxSlices; ++sl) s += t[sl];
+    sred[i] = s;  // the per-wave partials are no longer needed
+  }
+  __syncthreads();
+  for (int n = tid; n < rows; n += kThreads) {
+    float best = 0.0f;
+    int best_k = 0;
+    for (int k = 0; k < K; ++k) {
+      const float s = sred[n * K + k];
+      if (scores) scores[(int64_t)(n0 + n) * K + k] = s;
+      if (k == 0 || s > best) {
+        best = s;
+        best_k = k;
+      }
+    }
+    labels[n0 + n] = best_k;
+  }
+  if (tid == 0) reset_counter(ws.counters + tile);
+}
+
 // ---------------------------------------------------------------------------
 // The fused kernel.
 // ---------------------------------------------------------------------------
@@ -533,82 +628,203 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
       for (int t = 0; t < NTILES; ++t) cf.apply(vacc[b][t], b, sacc[t], act);
   }
 
-  // ---- combine the waves' partial scores through LDS -----------------------
-  __syncthreads();  // X tile no longer needed
-  float* sred = reinterpret_cast<float*>(lds);  // [kWaves][NT][32*KB]
-  constexpr int KP = 32 * KB;
+  finish_tile<NTILES, KB>(sacc, lds, &s_last, labels, scores, N, K, DS, ntiles, slice, tile, n0,
+                          workspace);
+}
+
+// ---------------------------------------------------------------------------
+// F-chunked variant, for feature counts whose X tile does not fit in LDS
+// (e.g. F = 3072). The workgroup walks its units in lockstep iterations, one
+// unit per wave each; an iteration streams the tile's X through LDS in chunks
+// of fsc f-steps and accumulates each wave's V^T over every chunk in
+// registers before Stage II, so H still never leaves the chip. X is read
+// again (from L2 or the last-level cache) once per iteration.
+// ---------------------------------------------------------------------------
+template <class Tr, int NTILES, int KB>
+__global__ __launch_bounds__(kThreads, 1) void large_chunked_kernel(
+    const typename Tr::elem* __restrict__ X, const uint4* __restrict__ Bp,
+    const uint4* __restrict__ Cp, int32_t* __restrict__ labels, float* __restrict__ scores,
+    int N, int F, int K, int ndb, int DS, int act, int fsc, void* __restrict__ workspace) {
+  typedef typename Tr::elem T;
+  constexpr int NT = 32 * NTILES;
+  constexpr int kPrefetch = kPrefetchMin;
+  constexpr int kSB = 8;  // staging items per thread per batch
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nfs = nfs_of<Tr>(F);
+  const int nchunks = (nfs + fsc - 1) / fsc;
+  const int pitch = fsc * Tr::kFStep + (Tr::kEsz == 2 ? 8 : 4);  // elements
+  const int ntiles = (int)cdiv(N, NT);
+  const int slice = blockIdx.x % DS;
+  const int tile = blockIdx.x / DS;
+  const int n0 = tile * NT;
+  const int rows = min(NT, N - n0);
+  const int units = ndb / 2;
+  const int u_begin = (int)((int64_t)units * slice / DS);
+  const int u_end = (int)((int64_t)units * (slice + 1) / DS);
+
+  T* xt = reinterpret_cast<T*>(lds);
+  const T* xzero = xt + NT * pitch;  // 16-byte zero slot after the chunk tile
+
+  // Stage f-steps [fs0, fs0 + fsc) of the tile's rows into LDS, zero past F
+  // and past the last sample. A work item is one f-step of one row: two
+  // 16-byte groups of X in, two 16-byte LDS words out (fp32 interleaves the
+  // two groups into the even/odd order of lds_pos). Loads are issued in
+  // unconditional batches with addresses clamped into X and masked after.
+  const bool vec = (F % Tr::kVec) == 0 && ((uintptr_t)X % 16) == 0;
+  auto stage = [&](int fs0) {
+    const int fsn = min(fsc, nfs - fs0);
+    const int items = NT * fsn;
+    for (int base = 0; base < items; base += kThreads * kSB) {
+      uint4 w[kSB][2];
+#pragma unroll
+      for (int j = 0; j < kSB; ++j) {
+        const int i = base + j * kThreads + tid;
+        const int r = i / fsn, s = i - r * fsn;
+        const int rr = r < rows ? r : rows - 1;
+        const T* xr = X + (int64_t)(n0 + rr) * F;
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          const int c = (fs0 + s) * Tr::kFStep + g * Tr::kVec;
+          if (vec) {
+            const int cc = c < F ? c : F - Tr::kVec;
+            w[j][g] = *reinterpret_cast<const uint4*>(xr + cc);
+          } else {
+            uint32_t t[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int e = 0; e < Tr::kVec; ++e) {
+              const int ce = c + e < F ? c + e : F - 1;
+              const T x = xr[ce];
+              if constexpr (Tr::kEsz == 2)
+                t[e >> 1] |= (uint32_t)x << (16 * (e & 1));
+              else
+                t[e] = __float_as_uint(x);
+            }
+            w[j][g] = make_uint4(t[0], t[1], t[2], t[3]);
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kSB; ++j) {
+        const int i = base + j * kThreads + tid;
+        if (i >= items) break;
+        const int r = i / fsn, s = i - r * fsn;
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          const int c = (fs0 + s) * Tr::kFStep + g * Tr::kVec;
+          if (r >= rows || c >= F) {
+            w[j][g] = make_uint4(0u, 0u, 0u, 0u);
+          } else if (c + Tr::kVec > F) {  // ragged last group (F % kVec != 0)
+            uint32_t t[4] = {w[j][g].x, w[j][g].y, w[j][g].z, w[j][g].w};
+#pragma unroll
+            for (int e = 0; e < Tr::kVec; ++e)
+              if (c + e >= F) {
+                if constexpr (Tr::kEsz == 2)
+                  t[e >> 1] &= ~(0xffffu << (16 * (e & 1)));
+                else
+                  t[e] = 0u;
+              }
+            w[j][g] = make_uint4(t[0], t[1], t[2], t[3]);
+          }
+        }
+        uint4* dst = reinterpret_cast<uint4*>(xt + r * pitch + s * Tr::kFStep);
+        if constexpr (Tr::kEsz == 2) {
+          dst[0] = w[j][0];
+          dst[1] = w[j][1];
+        } else {
+          dst[0] = make_uint4(w[j][0].x, w[j][0].z, w[j][1].x, w[j][1].z);
+          dst[1] = make_uint4(w[j][0].y, w[j][0].w, w[j][1].y, w[j][1].w);
+        }
+      }
+    }
+  };
+
+  f32x16 sacc[NTILES][KB];
 #pragma unroll
   for (int t = 0; t < NTILES; ++t)
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int k = 32 * kb + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int n = 32 * t + (lane & 31);
-        sred[((int64_t)wave * NT + n) * KP + k] = sacc[t][kb][r];
-      }
-  __syncthreads();
-  const int rows = min(NT, N - n0);
-  if (DS == 1) {
-    for (int n = tid; n < rows; n += kThreads) {
-      float best = 0.0f;
-      int best_k = 0;
-      for (int k = 0; k < K; ++k) {
-        float s = 0.0f;
+      for (int r = 0; r < 16; ++r) sacc[t][kb][r] = 0.0f;
+
+  const int xrow = lane & 31, xhalf = lane >> 5;
+  const T* xlane = xt + xrow * pitch + xhalf * (Tr::kFStep / 2);
+  const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(Bp), 0, ndb * nfs * 1024, 0x00020000);
+  auto bfrag = [&](int uu, int fs, int b) -> uint4 {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         brsrc, ((2 * uu + b) * nfs + fs) * 1024 + lane * 16, 0, 0));
+  };
+
+  const int n_it = (u_end - u_begin + kWaves - 1) / kWaves;
+  for (int it = 0; it < n_it; ++it) {
+    const int u = u_begin + wave + it * kWaves;
+    const bool valid = u < u_end;
+    const int uu = valid ? u : u_begin;  // waves without a unit compute and discard
+    CFrags<Tr, KB> cf;
+    cf.load(Cp, 2 * uu, lane);
+    f32x16 vacc[2][NTILES];
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) s += sred[((int64_t)w * NT + n) * KP + k];
-        if (scores) scores[(int64_t)(n0 + n) * K + k] = s;
-        if (k == 0 || s > best) {
-          best = s;
-          best_k = k;
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) vacc[b][t][r] = 0.0f;
+
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const int fs0 = ch * fsc;
+      const int fsn = min(fsc, nfs - fs0);  // f-steps of this chunk
+      __syncthreads();  // the previous chunk's readers are done
+      if (tid == 0) *reinterpret_cast<uint4*>(xt + NT * pitch) = make_uint4(0u, 0u, 0u, 0u);
+      stage(fs0);
+      __syncthreads();
+      uint4 afr[kPrefetch][2];
+#pragma unroll
+      for (int i = 0; i < kPrefetch; ++i) {
+        afr[i][0] = bfrag(uu, fs0 + (i < fsn ? i : fsn - 1), 0);
+        afr[i][1] = bfrag(uu, fs0 + (i < fsn ? i : fsn - 1), 1);
+      }
+      uint4 xfr[2][NTILES];
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t)
+        xfr[0][t] = *reinterpret_cast<const uint4*>(xlane + t * 32 * pitch);
+      const int fsl = (fsn + kPrefetch - 1) / kPrefetch * kPrefetch;
+      // Same branch-free step as the resident kernel: padding steps past fsn
+      // multiply a valid B fragment by the zero slot.
+      for (int s0 = 0; s0 < fsl; s0 += kPrefetch) {
+#pragma unroll
+        for (int i = 0; i < kPrefetch; ++i) {
+          const int fs = s0 + i;
+          const int fsx = fs + 1;
+#pragma unroll
+          for (int t = 0; t < NTILES; ++t)
+            xfr[(i + 1) & 1][t] = *reinterpret_cast<const uint4*>(
+                fsx < fsn ? xlane + t * 32 * pitch + fsx * Tr::kFStep : xzero);
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
+          __builtin_amdgcn_sched_group_barrier(0x100, NTILES, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES * Tr::kStage1Mfma, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+          const int nx = fs + kPrefetch;
+          afr[i][0] = bfrag(uu, fs0 + (nx < fsn ? nx : fsn - 1), 0);
+          afr[i][1] = bfrag(uu, fs0 + (nx < fsn ? nx : fsn - 1), 1);
         }
       }
-      labels[n0 + n] = best_k;
     }
-    return;
-  }
-  // Split-D: publish this slice's partial, the last slice of the tile finishes
-  // (summing the slices in a fixed order, so results are deterministic).
-  const LargeWs ws = large_ws(workspace, ntiles);
-  float* mypart = ws.part + (int64_t)slice * N * K;
-  for (int i = tid; i < rows * K; i += kThreads) {
-    const int n = i / K, k = i - n * K;
-    float s = 0.0f;
+    if (valid) {
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) s += sred[((int64_t)w * NT + n) * KP + k];
-    publish_store(mypart + (int64_t)(n0 + n) * K + k, s);
-  }
-  wait_own_memory_ops();
-  __syncthreads();
-  if (tid == 0) s_last = (take_ticket(ws.counters + tile) == (unsigned)DS - 1) ? 1 : 0;
-  __syncthreads();
-  if (!s_last) return;
-  for (int i = tid; i < rows * K; i += kThreads) {
-    const int n = i / K, k = i - n * K;
-    float t[kMaxSlices];
+      for (int b = 0; b < 2; ++b)
 #pragma unroll
-    for (int sl = 0; sl < kMaxSlices; ++sl)
-      t[sl] = sl < DS ? take_and_clear(ws.part + ((int64_t)sl * N + n0 + n) * K + k) : 0.0f;
-    float s = 0.0f;
-#pragma unroll
-    for (int sl = 0; sl < kMaxSlices; ++sl) s += t[sl];
-    sred[i] = s;  // the per-wave partials are no longer needed
-  }
-  __syncthreads();
-  for (int n = tid; n < rows; n += kThreads) {
-    float best = 0.0f;
-    int best_k = 0;
-    for (int k = 0; k < K; ++k) {
-      const float s = sred[n * K + k];
-      if (scores) scores[(int64_t)(n0 + n) * K + k] = s;
-      if (k == 0 || s > best) {
-        best = s;
-        best_k = k;
-      }
+        for (int t = 0; t < NTILES; ++t) cf.apply(vacc[b][t], b, sacc[t], act);
     }
-    labels[n0 + n] = best_k;
   }
-  if (tid == 0) reset_counter(ws.counters + tile);
+  __syncthreads();  // the last chunk's readers are done before LDS is reused
+  finish_tile<NTILES, KB>(sacc, lds, &s_last, labels, scores, N, K, DS, ntiles, slice, tile, n0,
+                          workspace);
 }
 
 // ---------------------------------------------------------------------------
@@ -617,6 +833,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
 struct LargeCfg {
   int ntiles_per_wg;  // NTILES
   int kb;
+  int fsc;            // f-steps per X chunk; 0 = the whole X tile stays in LDS
   int ds;
   int64_t ntiles;      // sample tiles
   size_t lds;
@@ -642,7 +859,19 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
       break;
     }
   }
-  if (!c.ntiles_per_wg) return c;
+  if (!c.ntiles_per_wg) {
+    // X tile too large for LDS: stream it in chunks of f-steps
+    const int nt = chunk_ntiles<Tr>(kbr);
+    const size_t rbytes = (size_t)kWaves * 32 * nt * 32 * kbr * 4;
+    const int pad = Tr::kEsz == 2 ? 8 : 4;
+    const int64_t cols = ((int64_t)kLdsBytes - 16) / (32 * nt * Tr::kEsz) - pad;
+    const int fsc = (int)(cols / Tr::kFStep);
+    if (fsc < 8 || rbytes > (size_t)kLdsBytes) return c;
+    c.ntiles_per_wg = nt;
+    c.fsc = fsc;
+    const size_t xbytes = (size_t)32 * nt * (fsc * Tr::kFStep + pad) * Tr::kEsz + 16;
+    c.lds = xbytes > rbytes ? xbytes : rbytes;
+  }
   c.kb = kbr;
   c.ntiles = cdiv(N, 32 * c.ntiles_per_wg);
   // Split D when there are too few sample tiles to give every CU a workgroup.
@@ -659,6 +888,19 @@ hipError_t launch_cfg(const LargeCfg& c, const void* X, const uint4* Bp, const u
                       int32_t* labels, float* scores, int64_t N, int64_t F, int64_t K, int ndb,
                       int act, void* ws, hipStream_t stream) {
   const dim3 grid((unsigned)(c.ntiles * c.ds)), block(kThreads);
+  if (c.fsc > 0) {
+    if constexpr (NTILES == chunk_ntiles<Tr>(KB)) {
+      static const hipError_t cattr = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(&large_chunked_kernel<Tr, NTILES, KB>),
+          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+      if (cattr != hipSuccess) return cattr;
+      hipLaunchKernelGGL((large_chunked_kernel<Tr, NTILES, KB>), grid, block, c.lds, stream,
+                         (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F,
+                         (int)K, ndb, c.ds, act, c.fsc, ws);
+      return hipGetLastError();
+    }
+    return hipErrorInvalidValue;
+  }
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(&large_fused_kernel<Tr, NTILES, KB>),
       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
@@ -698,6 +940,12 @@ hipError_t launch_tr(const void* X, const void* packed, int32_t* labels, float* 
 
 bool large_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   return dt == 0 ? large_cfg<TrF32>(N, F, D, K).ok : large_cfg<TrBF16>(N, F, D, K).ok;
+}
+
+const char* large_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  const LargeCfg c = dt == 0 ? large_cfg<TrF32>(N, F, D, K) : large_cfg<TrBF16>(N, F, D, K);
+  if (!c.ok) return "";
+  return c.fsc > 0 ? "large_chunked_kernel" : "large_fused_kernel";
 }
 
 size_t large_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {

@@ -92,6 +92,42 @@ def test_speech_workload_sampled(hd):
     assert drift.max() <= BF16_DRIFT, drift.max()
 
 
+@pytest.mark.parametrize("name,dtype", [("colour_k10", "bf16"), ("colour_k100", "bf16"),
+                                        ("colour_k10", "f32")])
+def test_colour_workload_sampled(hd, name, dtype):
+    torch = torch_or_skip()
+    w = hd_inputs.WORKLOADS[name]
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    assert hd.infer_kernel(w.N, w.F, w.D, w.K, tdt) == "large_chunked_kernel"
+    announce(f"{name} {dtype} N={w.N} F={w.F}")
+    X, B, C = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype=dtype)
+    y, S = run(hd, X, B, C, dtype, packed=True)
+    rows = np.r_[0:24, 8180:8200, w.N - 24:w.N, np.random.default_rng(3).integers(0, w.N, 40)]
+    rep, _ = check_against_oracle(X, B, C, y, S, rows=rows)
+    assert rep["ok"], rep
+
+
+# --- wide features: the X tile streamed through LDS in chunks ---------------
+
+CHUNKED = [(200, 3000, 300, 10, "bf16"), (130, 2999, 200, 7, "bf16"),
+           (70, 2600, 130, 100, "bf16"), (150, 1300, 256, 5, "f32"),
+           (90, 1283, 200, 40, "f32"), (65, 1500, 100, 70, "f32"),
+           (257, 5000, 640, 3, "bf16"), (129, 2560, 64, 33, "bf16")]
+
+
+@pytest.mark.parametrize("N,F,D,K,dtype", CHUNKED)
+def test_wide_features_chunked(hd, N, F, D, K, dtype):
+    torch = torch_or_skip()
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    assert hd.infer_kernel(N, F, D, K, tdt) == "large_chunked_kernel"
+    announce(f"chunked {dtype} N={N} F={F} D={D} K={K}")
+    X, B, C = inputs(N, F, D, K, "normal", seed=F + K, dtype=dtype)
+    for packed in (False, True):
+        y, S = run(hd, X, B, C, dtype, packed=packed)
+        rep, _ = check_against_oracle(X, B, C, y, S)
+        assert rep["ok"], (packed, rep)
+
+
 # --- exactness on small-integer inputs --------------------------------------
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
