@@ -34,7 +34,8 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kPrefetchMin = 4;  // f-steps of B fragments in flight per wave
+// f-steps of B fragments in flight per wave: deeper while registers allow
+constexpr int prefetch_of(int ntiles, int kb) { return ntiles * kb <= 4 ? 8 : 4; }
 constexpr int kMaxSlices = 16;  // D slices per sample tile (split-D)
 constexpr int kLdsBytes = 160 * 1024 - 256;  // leave room for static LDS
 
@@ -126,7 +127,7 @@ inline int kb_of(int64_t K) {
 // fit in registers, fewer as class blocks grow.
 template <class Tr>
 constexpr int chunk_ntiles(int kb) {
-  return kb > 2 ? 1 : (kb == 2 && Tr::kEsz == 4) ? 2 : 4;
+  return kb > 2 ? 1 : kb == 2 ? 2 : 4;
 }
 
 template <class Tr>
@@ -232,12 +233,12 @@ __device__ __forceinline__ uint32_t sign_pair(float a, float b) {
   return lo | (hi << 16);
 }
 
-template <int KB>
+template <int KB, int ACT>
 __device__ __forceinline__ void stage2_bf16(const f32x16& v, const uint4 (&cfr)[2][KB],
-                                            f32x16 (&s)[KB], int act) {
+                                            f32x16 (&s)[KB]) {
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    if (!act) {
+    if constexpr (ACT == 0) {
       uint4 hb;
       hb.x = sign_pair(v[8 * h + 0], v[8 * h + 1]);
       hb.y = sign_pair(v[8 * h + 2], v[8 * h + 3]);
@@ -274,14 +275,14 @@ __device__ __forceinline__ void stage2_bf16(const f32x16& v, const uint4 (&cfr)[
   }
 }
 
-template <int KB>
+template <int KB, int ACT>
 __device__ __forceinline__ void stage2_f32(const f32x16& v, const uint4 (&cfr)[KB][4],
-                                           f32x16 (&s)[KB], int act) {
+                                           f32x16 (&s)[KB]) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const float h = act ? v[4 * q + j] : hardsign(v[4 * q + j]);
+      const float h = ACT ? v[4 * q + j] : hardsign(v[4 * q + j]);
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
         const float c = __uint_as_float(j == 0 ? cfr[kb][q].x
@@ -309,8 +310,9 @@ struct CFrags<TrBF16, KB> {
         for (int kb = 0; kb < KB; ++kb)
           f[b][h][kb] = Cp[((int64_t)((db0 + b) * 2 + h) * KB + kb) * 64 + lane];
   }
-  __device__ void apply(const f32x16& v, int b, f32x16 (&s)[KB], int act) const {
-    stage2_bf16<KB>(v, f[b], s, act);
+  template <int ACT>
+  __device__ void apply(const f32x16& v, int b, f32x16 (&s)[KB]) const {
+    stage2_bf16<KB, ACT>(v, f[b], s);
   }
 };
 template <int KB>
@@ -325,8 +327,9 @@ struct CFrags<TrF32, KB> {
         for (int q = 0; q < 4; ++q)
           f[b][kb][q] = Cp[(((int64_t)(db0 + b) * KB + kb) * 4 + q) * 64 + lane];
   }
-  __device__ void apply(const f32x16& v, int b, f32x16 (&s)[KB], int act) const {
-    stage2_f32<KB>(v, f[b], s, act);
+  template <int ACT>
+  __device__ void apply(const f32x16& v, int b, f32x16 (&s)[KB]) const {
+    stage2_f32<KB, ACT>(v, f[b], s);
   }
 };
 
@@ -434,14 +437,14 @@ __device__ void finish_tile(f32x16 (&sacc)[NTILES][KB], unsigned char* lds, int*
 // ---------------------------------------------------------------------------
 // The fused kernel.
 // ---------------------------------------------------------------------------
-template <class Tr, int NTILES, int KB>
+template <class Tr, int NTILES, int KB, int ACT>
 __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     const typename Tr::elem* __restrict__ X, const uint4* __restrict__ Bp,
     const uint4* __restrict__ Cp, int32_t* __restrict__ labels, float* __restrict__ scores,
-    int N, int F, int K, int ndb, int DS, int act, void* __restrict__ workspace) {
+    int N, int F, int K, int ndb, int DS, void* __restrict__ workspace) {
   typedef typename Tr::elem T;
   constexpr int NT = 32 * NTILES;
-  constexpr int kPrefetch = kPrefetchMin;
+  constexpr int kPrefetch = prefetch_of(NTILES, KB);
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   __shared__ int s_last;
 
@@ -625,7 +628,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int t = 0; t < NTILES; ++t) cf.apply(vacc[b][t], b, sacc[t], act);
+      for (int t = 0; t < NTILES; ++t) cf.template apply<ACT>(vacc[b][t], b, sacc[t]);
   }
 
   finish_tile<NTILES, KB>(sacc, lds, &s_last, labels, scores, N, K, DS, ntiles, slice, tile, n0,
@@ -640,14 +643,14 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
 // registers before Stage II, so H still never leaves the chip. X is read
 // again (from L2 or the last-level cache) once per iteration.
 // ---------------------------------------------------------------------------
-template <class Tr, int NTILES, int KB>
+template <class Tr, int NTILES, int KB, int ACT>
 __global__ __launch_bounds__(kThreads, 1) void large_chunked_kernel(
     const typename Tr::elem* __restrict__ X, const uint4* __restrict__ Bp,
     const uint4* __restrict__ Cp, int32_t* __restrict__ labels, float* __restrict__ scores,
-    int N, int F, int K, int ndb, int DS, int act, int fsc, void* __restrict__ workspace) {
+    int N, int F, int K, int ndb, int DS, int fsc, void* __restrict__ workspace) {
   typedef typename Tr::elem T;
   constexpr int NT = 32 * NTILES;
-  constexpr int kPrefetch = kPrefetchMin;
+  constexpr int kPrefetch = prefetch_of(NTILES, KB);
   constexpr int kSB = 8;  // staging items per thread per batch
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   __shared__ int s_last;
@@ -819,10 +822,194 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_kernel(
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int t = 0; t < NTILES; ++t) cf.apply(vacc[b][t], b, sacc[t], act);
+        for (int t = 0; t < NTILES; ++t) cf.template apply<ACT>(vacc[b][t], b, sacc[t]);
     }
   }
   __syncthreads();  // the last chunk's readers are done before LDS is reused
+  finish_tile<NTILES, KB>(sacc, lds, &s_last, labels, scores, N, K, DS, ntiles, slice, tile, n0,
+                          workspace);
+}
+
+// LDS fragment reads of the double-buffered kernel. With buffer-to-LDS loads
+// in flight the compiler would put a full vmcnt(0) wait before every LDS
+// read it cannot prove disjoint from them; these reads are issued directly
+// and completed by an explicit lgkmcnt(0) tied to the destination registers.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 lds_read16_issue(uint32_t addr) {
+  u32x4_t v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return __builtin_bit_cast(uint4, v);
+}
+template <int NT>
+__device__ __forceinline__ void lds_reads_complete(uint4 (&v)[NT]) {
+  u32x4_t a = __builtin_bit_cast(u32x4_t, v[0]);
+  u32x4_t b = __builtin_bit_cast(u32x4_t, v[NT > 1 ? 1 : 0]);
+  u32x4_t c = __builtin_bit_cast(u32x4_t, v[NT > 2 ? 2 : 0]);
+  u32x4_t d = __builtin_bit_cast(u32x4_t, v[NT > 3 ? 3 : 0]);
+  if constexpr (NT == 1)
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a));
+  else if constexpr (NT == 2)
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b));
+  else
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d));
+  v[0] = __builtin_bit_cast(uint4, a);
+  if constexpr (NT > 1) v[1] = __builtin_bit_cast(uint4, b);
+  if constexpr (NT > 2) v[2] = __builtin_bit_cast(uint4, c);
+  if constexpr (NT > 3) v[3] = __builtin_bit_cast(uint4, d);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 F-chunked variant with the X chunks double-buffered in LDS and filled
+// by direct buffer-to-LDS loads (lane l of a 16-byte load lands at the wave's
+// LDS base + 16 l; out-of-range offsets deliver zeros). The loads of the next
+// chunk are spread over the f-steps of the current one, one per step, so they
+// overlap the matrix instructions instead of stalling the workgroup.
+// An LDS row is W = 2 fsc + 1 slots of 16 bytes: two per f-step plus one
+// padding slot that keeps the 32 rows of a fragment read on distinct banks.
+// Requires F % 8 == 0 and a 16-byte aligned X.
+// ---------------------------------------------------------------------------
+template <int NTILES, int KB, int ACT>
+__global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
+    const bf16raw* __restrict__ X, const uint4* __restrict__ Bp, const uint4* __restrict__ Cp,
+    int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int K, int ndb,
+    int DS, int fsc, void* __restrict__ workspace) {
+  typedef TrBF16 Tr;
+  constexpr int NT = 32 * NTILES;
+  constexpr int kPrefetch = prefetch_of(NTILES, KB);
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nfs = nfs_of<Tr>(F);
+  const int nchunks = (nfs + fsc - 1) / fsc;
+  const int W = 2 * fsc + 1;                                  // slots per LDS row
+  const int pitch = 8 * W;                                    // elements
+  const int P = (NT * W + kThreads - 1) / kThreads;           // loads per wave per chunk
+  const int buf_elems = P * kThreads * 8;
+  const int ntiles = (int)cdiv(N, NT);
+  const int slice = blockIdx.x % DS;
+  const int tile = blockIdx.x / DS;
+  const int n0 = tile * NT;
+  const int rows = min(NT, N - n0);
+  const int units = ndb / 2;
+  const int u_begin = (int)((int64_t)units * slice / DS);
+  const int u_end = (int)((int64_t)units * (slice + 1) / DS);
+
+  bf16raw* xb = reinterpret_cast<bf16raw*>(lds);  // two buffers of buf_elems
+  const bf16raw* xzero = xb + 2 * buf_elems;      // 16-byte zero slot
+  if (tid == 0) *reinterpret_cast<uint4*>(xb + 2 * buf_elems) = make_uint4(0u, 0u, 0u, 0u);
+
+  // The tile's rows of X as one buffer resource; rows past N are out of range.
+  const __amdgpu_buffer_rsrc_t xrsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16raw*>(X + (int64_t)n0 * F), 0, rows * F * 2, 0x00020000);
+  // Load p of this wave for chunk ch into buffer `buf`: slot q of the buffer.
+  auto dma = [&](int ch, int p, int buf) {
+    const int q = (p * kWaves + wave) * 64 + lane;
+    const int r = q / W, rem = q - r * W;
+    const int col = (ch * fsc + (rem >> 1)) * 16 + (rem & 1) * 8;
+    const bool ok = r < rows && rem < 2 * fsc && col < F;
+    const unsigned off = ok ? (unsigned)((r * F + col) * 2) : 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        xrsrc,
+        (__attribute__((address_space(3))) void*)(xb + buf * buf_elems +
+                                                  (p * kWaves + wave) * 64 * 8),
+        16, off, 0, 0, 0);
+  };
+
+  f32x16 sacc[NTILES][KB];
+#pragma unroll
+  for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[t][kb][r] = 0.0f;
+
+  const int xrow = lane & 31, xhalf = lane >> 5;
+  const int xlane = xrow * pitch + xhalf * (Tr::kFStep / 2);  // element offset in a buffer
+  const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(Bp), 0, ndb * nfs * 1024, 0x00020000);
+  auto bfrag = [&](int uu, int fs, int b) -> uint4 {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         brsrc, ((2 * uu + b) * nfs + fs) * 1024 + lane * 16, 0, 0));
+  };
+
+  for (int p = 0; p < P; ++p) dma(0, p, 0);
+  int cur = 0;
+  const int n_it = (u_end - u_begin + kWaves - 1) / kWaves;
+  for (int it = 0; it < n_it; ++it) {
+    const int u = u_begin + wave + it * kWaves;
+    const bool valid = u < u_end;
+    const int uu = valid ? u : u_begin;
+    CFrags<Tr, KB> cf;
+    cf.load(Cp, 2 * uu, lane);
+    f32x16 vacc[2][NTILES];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) vacc[b][t][r] = 0.0f;
+
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const int fs0 = ch * fsc;
+      const int fsn = min(fsc, nfs - fs0);
+      const int nch = ch + 1 < nchunks ? ch + 1 : 0;  // the next chunk to fill
+      // This wave's loads of chunk ch are done; after the barrier every
+      // wave's are, and nobody still reads the other buffer.
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+      __syncthreads();
+      const uint32_t xc = lds_addr(xb + cur * buf_elems + xlane);
+      const uint32_t xz = lds_addr(xzero);
+      const int nbuf = cur ^ 1;
+      uint4 afr[kPrefetch][2];
+#pragma unroll
+      for (int i = 0; i < kPrefetch; ++i) {
+        afr[i][0] = bfrag(uu, fs0 + (i < fsn ? i : fsn - 1), 0);
+        afr[i][1] = bfrag(uu, fs0 + (i < fsn ? i : fsn - 1), 1);
+      }
+      uint4 xfr[2][NTILES];
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t) xfr[0][t] = lds_read16_issue(xc + t * 64 * pitch);
+      const int fsl = (fsn + kPrefetch - 1) / kPrefetch * kPrefetch;
+      for (int s0 = 0; s0 < fsl; s0 += kPrefetch) {
+#pragma unroll
+        for (int i = 0; i < kPrefetch; ++i) {
+          const int fs = s0 + i;
+          const int fsx = fs + 1;
+          lds_reads_complete<NTILES>(xfr[i & 1]);
+#pragma unroll
+          for (int t = 0; t < NTILES; ++t)
+            xfr[(i + 1) & 1][t] =
+                lds_read16_issue(fsx < fsn ? xc + t * 64 * pitch + fsx * 32 : xz);
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 3, 0);
+          const int nx = fs + kPrefetch;
+          afr[i][0] = bfrag(uu, fs0 + (nx < fsn ? nx : fsn - 1), 0);
+          afr[i][1] = bfrag(uu, fs0 + (nx < fsn ? nx : fsn - 1), 1);
+          dma(nch, fs < P ? fs : P - 1, nbuf);  // repeats of the last load are harmless
+        }
+      }
+      // the reads issued by the last step (of padding) complete before reuse
+      lds_reads_complete<NTILES>(xfr[fsl & 1]);
+      for (int p = fsl; p < P; ++p) dma(nch, p, nbuf);
+      cur = nbuf;
+    }
+    if (valid) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int t = 0; t < NTILES; ++t) cf.template apply<ACT>(vacc[b][t], b, sacc[t]);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // no load into LDS is still in flight
+  __syncthreads();
   finish_tile<NTILES, KB>(sacc, lds, &s_last, labels, scores, N, K, DS, ntiles, slice, tile, n0,
                           workspace);
 }
@@ -834,6 +1021,7 @@ struct LargeCfg {
   int ntiles_per_wg;  // NTILES
   int kb;
   int fsc;            // f-steps per X chunk; 0 = the whole X tile stays in LDS
+  bool dma;           // chunks double-buffered by buffer-to-LDS loads (bf16)
   int ds;
   int64_t ntiles;      // sample tiles
   size_t lds;
@@ -841,7 +1029,7 @@ struct LargeCfg {
 };
 
 template <class Tr>
-LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
+LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) {
   LargeCfg c{};
   if (cdiv(K, 32) > 4 || F > (1 << 20) || N > (1 << 30)) return c;
   // B fragments are addressed with 32-bit byte offsets
@@ -871,6 +1059,19 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
     c.fsc = fsc;
     const size_t xbytes = (size_t)32 * nt * (fsc * Tr::kFStep + pad) * Tr::kEsz + 16;
     c.lds = xbytes > rbytes ? xbytes : rbytes;
+    if (Tr::kEsz == 2 && F % 8 == 0 && x16) {
+      // two buffers of P * kThreads slots of 16 bytes, plus the zero slot
+      const int pmax = (kLdsBytes - 16) / (2 * kThreads * 16);
+      const int w = pmax * kThreads / (32 * nt);
+      const int dfsc = (w - 1) / 2;
+      if (dfsc >= 8) {
+        const int P = (32 * nt * (2 * dfsc + 1) + kThreads - 1) / kThreads;
+        const size_t dbytes = (size_t)2 * P * kThreads * 16 + 16;
+        c.dma = true;
+        c.fsc = dfsc;
+        c.lds = dbytes > rbytes ? dbytes : rbytes;
+      }
+    }
   }
   c.kb = kbr;
   c.ntiles = cdiv(N, 32 * c.ntiles_per_wg);
@@ -883,39 +1084,61 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
   return c;
 }
 
-template <class Tr, int NTILES, int KB>
-hipError_t launch_cfg(const LargeCfg& c, const void* X, const uint4* Bp, const uint4* Cp,
+template <class Tr, int NTILES, int KB, int ACT>
+hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const uint4* Cp,
                       int32_t* labels, float* scores, int64_t N, int64_t F, int64_t K, int ndb,
-                      int act, void* ws, hipStream_t stream) {
+                      void* ws, hipStream_t stream) {
   const dim3 grid((unsigned)(c.ntiles * c.ds)), block(kThreads);
   if (c.fsc > 0) {
     if constexpr (NTILES == chunk_ntiles<Tr>(KB)) {
+      if (c.dma) {
+        if constexpr (Tr::kEsz == 2) {
+          static const hipError_t dattr = hipFuncSetAttribute(
+              reinterpret_cast<const void*>(&large_chunked_dma_kernel<NTILES, KB, ACT>),
+              hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+          if (dattr != hipSuccess) return dattr;
+          hipLaunchKernelGGL((large_chunked_dma_kernel<NTILES, KB, ACT>), grid, block, c.lds,
+                             stream, (const bf16raw*)X, Bp, Cp, labels, scores, (int)N, (int)F,
+                             (int)K, ndb, c.ds, c.fsc, ws);
+          return hipGetLastError();
+        }
+        return hipErrorInvalidValue;
+      }
       static const hipError_t cattr = hipFuncSetAttribute(
-          reinterpret_cast<const void*>(&large_chunked_kernel<Tr, NTILES, KB>),
+          reinterpret_cast<const void*>(&large_chunked_kernel<Tr, NTILES, KB, ACT>),
           hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
       if (cattr != hipSuccess) return cattr;
-      hipLaunchKernelGGL((large_chunked_kernel<Tr, NTILES, KB>), grid, block, c.lds, stream,
+      hipLaunchKernelGGL((large_chunked_kernel<Tr, NTILES, KB, ACT>), grid, block, c.lds, stream,
                          (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F,
-                         (int)K, ndb, c.ds, act, c.fsc, ws);
+                         (int)K, ndb, c.ds, c.fsc, ws);
       return hipGetLastError();
     }
     return hipErrorInvalidValue;
   }
   static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&large_fused_kernel<Tr, NTILES, KB>),
+      reinterpret_cast<const void*>(&large_fused_kernel<Tr, NTILES, KB, ACT>),
       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((large_fused_kernel<Tr, NTILES, KB>), grid, block, c.lds, stream,
+  hipLaunchKernelGGL((large_fused_kernel<Tr, NTILES, KB, ACT>), grid, block, c.lds, stream,
                      (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F, (int)K,
-                     ndb, c.ds, act, ws);
+                     ndb, c.ds, ws);
   return hipGetLastError();
+}
+
+template <class Tr, int NTILES, int KB>
+hipError_t launch_cfg(const LargeCfg& c, const void* X, const uint4* Bp, const uint4* Cp,
+                      int32_t* labels, float* scores, int64_t N, int64_t F, int64_t K, int ndb,
+                      int act, void* ws, hipStream_t stream) {
+  if (act)
+    return launch_act<Tr, NTILES, KB, 1>(c, X, Bp, Cp, labels, scores, N, F, K, ndb, ws, stream);
+  return launch_act<Tr, NTILES, KB, 0>(c, X, Bp, Cp, labels, scores, N, F, K, ndb, ws, stream);
 }
 
 template <class Tr>
 hipError_t launch_tr(const void* X, const void* packed, int32_t* labels, float* scores,
                      int64_t N, int64_t F, int64_t D, int64_t K, int act, void* ws,
                      hipStream_t stream) {
-  const LargeCfg c = large_cfg<Tr>(N, F, D, K);
+  const LargeCfg c = large_cfg<Tr>(N, F, D, K, ((uintptr_t)X % 16) == 0);
   if (!c.ok) return hipErrorInvalidValue;
   const PackGeom g = pack_geom<Tr>(F, D, K);
   const uint4* Bp = (const uint4*)packed;
@@ -945,7 +1168,8 @@ bool large_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
 const char* large_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   const LargeCfg c = dt == 0 ? large_cfg<TrF32>(N, F, D, K) : large_cfg<TrBF16>(N, F, D, K);
   if (!c.ok) return "";
-  return c.fsc > 0 ? "large_chunked_kernel" : "large_fused_kernel";
+  if (c.fsc > 0) return c.dma ? "large_chunked_dma_kernel" : "large_chunked_kernel";
+  return "large_fused_kernel";
 }
 
 size_t large_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {

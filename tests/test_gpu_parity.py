@@ -98,7 +98,7 @@ def test_colour_workload_sampled(hd, name, dtype):
     torch = torch_or_skip()
     w = hd_inputs.WORKLOADS[name]
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    assert hd.infer_kernel(w.N, w.F, w.D, w.K, tdt) == "large_chunked_kernel"
+    assert hd.infer_kernel(w.N, w.F, w.D, w.K, tdt).startswith("large_chunked")
     announce(f"{name} {dtype} N={w.N} F={w.F}")
     X, B, C = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype=dtype)
     y, S = run(hd, X, B, C, dtype, packed=True)
@@ -109,23 +109,51 @@ def test_colour_workload_sampled(hd, name, dtype):
 
 # --- wide features: the X tile streamed through LDS in chunks ---------------
 
-CHUNKED = [(200, 3000, 300, 10, "bf16"), (130, 2999, 200, 7, "bf16"),
-           (70, 2600, 130, 100, "bf16"), (150, 1300, 256, 5, "f32"),
-           (90, 1283, 200, 40, "f32"), (65, 1500, 100, 70, "f32"),
-           (257, 5000, 640, 3, "bf16"), (129, 2560, 64, 33, "bf16")]
+# (N, F, D, K, dtype, kernel): bf16 with F % 8 == 0 double-buffers the chunks
+# through buffer-to-LDS loads; ragged F and fp32 stage them through registers.
+CHUNKED = [(200, 3000, 300, 10, "bf16", "dma"), (130, 2999, 200, 7, "bf16", ""),
+           (70, 2600, 130, 100, "bf16", "dma"), (150, 1300, 256, 5, "f32", ""),
+           (90, 1283, 200, 40, "f32", ""), (65, 1500, 100, 70, "f32", ""),
+           (257, 5000, 640, 3, "bf16", "dma"), (129, 2560, 64, 33, "bf16", "dma"),
+           (300, 2568, 1000, 2, "bf16", "dma"), (66, 2602, 200, 50, "bf16", "")]
 
 
-@pytest.mark.parametrize("N,F,D,K,dtype", CHUNKED)
-def test_wide_features_chunked(hd, N, F, D, K, dtype):
+@pytest.mark.parametrize("N,F,D,K,dtype,kind", CHUNKED)
+def test_wide_features_chunked(hd, N, F, D, K, dtype, kind):
     torch = torch_or_skip()
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    assert hd.infer_kernel(N, F, D, K, tdt) == "large_chunked_kernel"
+    want = "large_chunked_dma_kernel" if kind == "dma" else "large_chunked_kernel"
+    assert hd.infer_kernel(N, F, D, K, tdt) == want
     announce(f"chunked {dtype} N={N} F={F} D={D} K={K}")
     X, B, C = inputs(N, F, D, K, "normal", seed=F + K, dtype=dtype)
     for packed in (False, True):
         y, S = run(hd, X, B, C, dtype, packed=packed)
         rep, _ = check_against_oracle(X, B, C, y, S)
         assert rep["ok"], (packed, rep)
+
+
+@pytest.mark.parametrize("N,F,dtype", [(150, 2600, "bf16"), (150, 2598, "bf16"), (70, 1300, "f32")])
+def test_wide_features_identity(hd, N, F, dtype):
+    announce(f"chunked identity {dtype} N={N} F={F}")
+    X, B, C = inputs(N, F, 500, 6, "normal", seed=9, dtype=dtype)
+    y, S = run(hd, X, B, C, dtype, act="identity")
+    rep, _ = check_against_oracle(X, B, C, y, S, act="identity")
+    assert rep["ok"], rep
+
+
+def test_wide_features_unaligned_x(hd):
+    """X at an offset that is not 16-byte aligned takes the register-staged kernel."""
+    torch = torch_or_skip()
+    N, F, D, K = 130, 2600, 300, 5
+    announce("chunked bf16 unaligned X")
+    X, B, C = inputs(N, F, D, K, "normal", seed=11, dtype="bf16")
+    Xd = dev(np.concatenate([np.zeros(1, np.float32), X.ravel()]), "bf16")[1:].view(N, F)
+    Bd, Cd = dev(B, "bf16"), dev(C, "bf16")
+    assert Xd.data_ptr() % 16 != 0
+    y, S = hd.infer(Xd, Bd, Cd, return_scores=True)
+    torch.cuda.synchronize()
+    rep, _ = check_against_oracle(X, B, C, y.cpu().numpy(), S.cpu().numpy().astype(np.float64))
+    assert rep["ok"], rep
 
 
 # --- exactness on small-integer inputs --------------------------------------
