@@ -127,7 +127,7 @@ inline int kb_of(int64_t K) {
 // fit in registers, fewer as class blocks grow.
 template <class Tr>
 constexpr int chunk_ntiles(int kb) {
-  return kb > 2 ? 1 : kb == 2 ? 2 : 4;
+  return kb > 2 ? (Tr::kEsz == 2 ? 2 : 1) : kb == 2 ? 2 : 4;
 }
 
 template <class Tr>
@@ -865,30 +865,47 @@ __device__ __forceinline__ void lds_reads_complete(uint4 (&v)[NT]) {
 // bf16 F-chunked variant with the X chunks double-buffered in LDS and filled
 // by direct buffer-to-LDS loads (lane l of a 16-byte load lands at the wave's
 // LDS base + 16 l; out-of-range offsets deliver zeros). The loads of the next
-// chunk are spread over the f-steps of the current one, one per step, so they
-// overlap the matrix instructions instead of stalling the workgroup.
-// An LDS row is W = 2 fsc + 1 slots of 16 bytes: two per f-step plus one
+// chunk are issued two per f-step at the start of the current one, so they
+// overlap the matrix instructions. Chunks are a fixed kDmaFsc f-steps (the
+// last one of a unit padded with zero X), which keeps the B fragment ring
+// running across chunk and unit boundaries, and lets the barrier that
+// publishes a chunk wait only for the LDS loads, not for the ring behind them.
+// An LDS row is W = 2 kDmaFsc + 1 slots of 16 bytes: two per f-step plus one
 // padding slot that keeps the 32 rows of a fragment read on distinct banks.
 // Requires F % 8 == 0 and a 16-byte aligned X.
 // ---------------------------------------------------------------------------
+constexpr int kDmaFsc = 16;
+
+__host__ __device__ constexpr int dma_loads_per_wave(int ntiles) {
+  return (32 * ntiles * (2 * kDmaFsc + 1) + kThreads - 1) / kThreads;
+}
+
 template <int NTILES, int KB, int ACT>
 __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
     const bf16raw* __restrict__ X, const uint4* __restrict__ Bp, const uint4* __restrict__ Cp,
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int K, int ndb,
-    int DS, int fsc, void* __restrict__ workspace) {
+    int DS, void* __restrict__ workspace) {
   typedef TrBF16 Tr;
   constexpr int NT = 32 * NTILES;
-  constexpr int kPrefetch = prefetch_of(NTILES, KB);
+  constexpr int kPF = prefetch_of(NTILES, KB);
+  constexpr int FSC = kDmaFsc;
+  constexpr int W = 2 * FSC + 1;                 // slots per LDS row
+  constexpr int pitch = 8 * W;                   // elements
+  constexpr int P = dma_loads_per_wave(NTILES);  // LDS loads per wave per chunk
+  constexpr int kDmaSteps = (P + 1) / 2;         // the first steps issue them, two each
+  constexpr int kAfter = 2 * (FSC - kDmaSteps);  // ring loads issued after the last one
+  constexpr int kWait = kAfter < 2 * kPF ? kAfter : 2 * kPF;
+  constexpr int buf_elems = P * kThreads * 8;
+  static_assert(FSC % kPF == 0 && kDmaSteps <= FSC && kWait <= 63, "chunk schedule");
+  // s_waitcnt immediate: vmcnt(kWait), expcnt and lgkmcnt not waited on
+  constexpr int kWaitImm = 0x0F70 | (kWait & 15) | ((kWait >> 4) << 14);
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nfs = nfs_of<Tr>(F);
-  const int nchunks = (nfs + fsc - 1) / fsc;
-  const int W = 2 * fsc + 1;                                  // slots per LDS row
-  const int pitch = 8 * W;                                    // elements
-  const int P = (NT * W + kThreads - 1) / kThreads;           // loads per wave per chunk
-  const int buf_elems = P * kThreads * 8;
+  const int nchunks = (nfs + FSC - 1) / FSC;
+  const int nfl = nchunks * FSC;  // f-steps per unit, padded to whole chunks
   const int ntiles = (int)cdiv(N, NT);
   const int slice = blockIdx.x % DS;
   const int tile = blockIdx.x / DS;
@@ -907,10 +924,13 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
       const_cast<bf16raw*>(X + (int64_t)n0 * F), 0, rows * F * 2, 0x00020000);
   // Load p of this wave for chunk ch into buffer `buf`: slot q of the buffer.
   auto dma = [&](int ch, int p, int buf) {
-    const int q = (p * kWaves + wave) * 64 + lane;
+    int q = (p * kWaves + wave) * 64 + lane;
+    // recomputed at each use: hoisting the per-load slot arithmetic out of
+    // the chunk loop would hold dozens of registers for the whole unit
+    asm volatile("" : "+v"(q));
     const int r = q / W, rem = q - r * W;
-    const int col = (ch * fsc + (rem >> 1)) * 16 + (rem & 1) * 8;
-    const bool ok = r < rows && rem < 2 * fsc && col < F;
+    const int col = (ch * FSC + (rem >> 1)) * 16 + (rem & 1) * 8;
+    const bool ok = r < rows && rem < 2 * FSC && col < F;
     const unsigned off = ok ? (unsigned)((r * F + col) * 2) : 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         xrsrc,
@@ -935,14 +955,28 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
                                          brsrc, ((2 * uu + b) * nfs + fs) * 1024 + lane * 16, 0, 0));
   };
+  // this wave's unit in iteration it (a valid unit when it has none: computed, discarded)
+  auto unit_of = [&](int it) {
+    const int u = u_begin + wave + it * kWaves;
+    return u < u_end ? u : u_begin;
+  };
 
   for (int p = 0; p < P; ++p) dma(0, p, 0);
+  // ring slot g % kPF holds f-step g of the current unit
+  uint4 afr[kPF][2];
+  {
+    const int u0 = unit_of(0);
+#pragma unroll
+    for (int i = 0; i < kPF; ++i) {
+      afr[i][0] = bfrag(u0, i < nfs ? i : nfs - 1, 0);
+      afr[i][1] = bfrag(u0, i < nfs ? i : nfs - 1, 1);
+    }
+  }
   int cur = 0;
   const int n_it = (u_end - u_begin + kWaves - 1) / kWaves;
   for (int it = 0; it < n_it; ++it) {
-    const int u = u_begin + wave + it * kWaves;
-    const bool valid = u < u_end;
-    const int uu = valid ? u : u_begin;
+    const bool valid = u_begin + wave + it * kWaves < u_end;
+    const int uu = unit_of(it), un = unit_of(it + 1);
     CFrags<Tr, KB> cf;
     cf.load(Cp, 2 * uu, lane);
     f32x16 vacc[2][NTILES];
@@ -954,51 +988,50 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
         for (int r = 0; r < 16; ++r) vacc[b][t][r] = 0.0f;
 
     for (int ch = 0; ch < nchunks; ++ch) {
-      const int fs0 = ch * fsc;
-      const int fsn = min(fsc, nfs - fs0);
+      const int fs0 = ch * FSC;
+      const int fsn = min(FSC, nfs - fs0);
       const int nch = ch + 1 < nchunks ? ch + 1 : 0;  // the next chunk to fill
-      // This wave's loads of chunk ch are done; after the barrier every
-      // wave's are, and nobody still reads the other buffer.
-      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+      // This wave's loads of chunk ch are done (only ring loads were issued
+      // after them); after the barrier every wave's are, and nobody still
+      // reads the other buffer.
+      __builtin_amdgcn_s_waitcnt(kWaitImm);
       __syncthreads();
       const uint32_t xc = lds_addr(xb + cur * buf_elems + xlane);
       const uint32_t xz = lds_addr(xzero);
       const int nbuf = cur ^ 1;
-      uint4 afr[kPrefetch][2];
-#pragma unroll
-      for (int i = 0; i < kPrefetch; ++i) {
-        afr[i][0] = bfrag(uu, fs0 + (i < fsn ? i : fsn - 1), 0);
-        afr[i][1] = bfrag(uu, fs0 + (i < fsn ? i : fsn - 1), 1);
-      }
       uint4 xfr[2][NTILES];
 #pragma unroll
       for (int t = 0; t < NTILES; ++t) xfr[0][t] = lds_read16_issue(xc + t * 64 * pitch);
-      const int fsl = (fsn + kPrefetch - 1) / kPrefetch * kPrefetch;
-      for (int s0 = 0; s0 < fsl; s0 += kPrefetch) {
 #pragma unroll
-        for (int i = 0; i < kPrefetch; ++i) {
-          const int fs = s0 + i;
-          const int fsx = fs + 1;
-          lds_reads_complete<NTILES>(xfr[i & 1]);
+      for (int s = 0; s < FSC; ++s) {
+        const int i = s % kPF;
+        lds_reads_complete<NTILES>(xfr[s & 1]);
 #pragma unroll
-          for (int t = 0; t < NTILES; ++t)
-            xfr[(i + 1) & 1][t] =
-                lds_read16_issue(fsx < fsn ? xc + t * 64 * pitch + fsx * 32 : xz);
+        for (int t = 0; t < NTILES; ++t)
+          xfr[(s + 1) & 1][t] =
+              lds_read16_issue(s + 1 < fsn ? xc + t * 64 * pitch + (s + 1) * 32 : xz);
 #pragma unroll
-          for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-            for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
-          __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES, 0);
-          __builtin_amdgcn_sched_group_barrier(0x020, 3, 0);
-          const int nx = fs + kPrefetch;
-          afr[i][0] = bfrag(uu, fs0 + (nx < fsn ? nx : fsn - 1), 0);
-          afr[i][1] = bfrag(uu, fs0 + (nx < fsn ? nx : fsn - 1), 1);
-          dma(nch, fs < P ? fs : P - 1, nbuf);  // repeats of the last load are harmless
+          for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[s & 1][t]);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES, 0);
+        if (s < kDmaSteps)
+          __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+        else
+          __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+        // refill: f-step g of this unit, else the next unit's first steps
+        const int g = fs0 + s + kPF;
+        const int ru = g < nfl ? uu : un;
+        const int rg0 = g < nfl ? g : g - nfl;
+        const int rg = rg0 < nfs ? rg0 : nfs - 1;
+        afr[i][0] = bfrag(ru, rg, 0);
+        afr[i][1] = bfrag(ru, rg, 1);
+        if (s < kDmaSteps) {
+          dma(nch, 2 * s < P ? 2 * s : P - 1, nbuf);  // a repeated load is harmless
+          dma(nch, 2 * s + 1 < P ? 2 * s + 1 : P - 1, nbuf);
         }
       }
-      // the reads issued by the last step (of padding) complete before reuse
-      lds_reads_complete<NTILES>(xfr[fsl & 1]);
-      for (int p = fsl; p < P; ++p) dma(nch, p, nbuf);
+      lds_reads_complete<NTILES>(xfr[FSC & 1]);  // the padding read of the last step
       cur = nbuf;
     }
     if (valid) {
@@ -1061,14 +1094,10 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) 
     c.lds = xbytes > rbytes ? xbytes : rbytes;
     if (Tr::kEsz == 2 && F % 8 == 0 && x16) {
       // two buffers of P * kThreads slots of 16 bytes, plus the zero slot
-      const int pmax = (kLdsBytes - 16) / (2 * kThreads * 16);
-      const int w = pmax * kThreads / (32 * nt);
-      const int dfsc = (w - 1) / 2;
-      if (dfsc >= 8) {
-        const int P = (32 * nt * (2 * dfsc + 1) + kThreads - 1) / kThreads;
-        const size_t dbytes = (size_t)2 * P * kThreads * 16 + 16;
+      const size_t dbytes = (size_t)2 * dma_loads_per_wave(nt) * kThreads * 16 + 16;
+      if (dbytes <= (size_t)kLdsBytes) {
         c.dma = true;
-        c.fsc = dfsc;
+        c.fsc = kDmaFsc;
         c.lds = dbytes > rbytes ? dbytes : rbytes;
       }
     }
@@ -1099,7 +1128,7 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
           if (dattr != hipSuccess) return dattr;
           hipLaunchKernelGGL((large_chunked_dma_kernel<NTILES, KB, ACT>), grid, block, c.lds,
                              stream, (const bf16raw*)X, Bp, Cp, labels, scores, (int)N, (int)F,
-                             (int)K, ndb, c.ds, c.fsc, ws);
+                             (int)K, ndb, c.ds, ws);
           return hipGetLastError();
         }
         return hipErrorInvalidValue;
