@@ -592,8 +592,11 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     // interleave the refill arithmetic with the matrix instructions and track
     // the wait counters across the loop. Padding steps past nfs (up to
     // kPrefetch-1 of them) multiply a valid, finite B fragment by the zero
-    // slot.
-    for (int fs0 = 0; fs0 < nfsl; fs0 += kPrefetch) {
+    // slot. The loop is a do-while (it always runs, nfsl >= kPrefetch): with
+    // a possible zero-trip path the compiler would make Stage II wait for
+    // every ring load in flight before using the C fragments loaded above.
+    int fs0 = 0;
+    do {
 #pragma unroll
       for (int i = 0; i < kPrefetch; ++i) {
         const int fs = fs0 + i;
@@ -623,7 +626,8 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
         afr[i][0] = bfrag(tu, tf, 0);
         afr[i][1] = bfrag(tu, tf, 1);
       }
-    }
+      fs0 += kPrefetch;
+    } while (fs0 < nfsl);
     // Stage II on the finished unit.
 #pragma unroll
     for (int b = 0; b < 2; ++b)
