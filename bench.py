@@ -8,10 +8,12 @@ line: whole-job samples/s, the roofline fraction of the dominant kernel
 and the CPU oracle's throughput on a bounded sample as a baseline.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+    python bench.py --sweep-d     # N = 1, F = 3072, K = 10: one line per D (bandwidth map)
 """
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -34,7 +36,7 @@ MALL_BYTES = 256 << 20
 
 # workload -> (dtype, path description)
 BENCH_DTYPE = {"activity_n1": "f32", "activity_n32": "f32", "tiny": "f32", "image": "bf16",
-               "speech": "bf16", "colour_k10": "bf16", "colour_k100": "bf16"}
+               "speech": "bf16", "colour_k10": "bf16", "colour_k100": "bf16", "colour_n1": "f32"}
 
 
 def parse():
@@ -50,6 +52,10 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--d", type=int, default=0, help="override the workload's D")
+    p.add_argument("--sweep-d", action="store_true",
+                   help="single-sample bandwidth map: one JSON line per D in hd_inputs.D_SWEEP "
+                        "for the colour_n1 shape (F=3072, K=10), no CPU baseline")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="after timing, run a plain device-to-device copy of this many MiB "
                         "(the reference kernel for scaling hardware byte counters)")
@@ -63,10 +69,22 @@ def main():
                                    "note only (split-N replicas or split-D with an all-reduce of "
                                    "partial scores)", "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.sweep_d:
+        args.workload, args.no_cpu_baseline = "colour_n1", True
+        base = hd_inputs.WORKLOADS["colour_n1"]
+        for d in hd_inputs.D_SWEEP:
+            run(args, dataclasses.replace(base, name=f"colour_n1_d{d}", D=d))
+        return
+    w = hd_inputs.WORKLOADS[args.workload]
+    if args.d:
+        w = dataclasses.replace(w, name=f"{w.name}_d{args.d}", D=args.d)
+    run(args, w)
+
+
+def run(args, w):
     import torch
     import paper_2506_09282_amd as hd
 
-    w = hd_inputs.WORKLOADS[args.workload]
     dtype = args.dtype or BENCH_DTYPE[args.workload]
     small = w.N <= 64
     steps = args.steps or (2000 if small else 100)

@@ -67,7 +67,12 @@ WORKLOADS = {
                            "colour-image-shaped, wide features"),
     "colour_k100": Workload("colour_k100", 16384, 3072, 10240, 100, "uniform01", ("bf16", "f32"),
                             "colour-image-shaped, 100 classes"),
+    "colour_n1": Workload("colour_n1", 1, 3072, 10240, 10, "uniform01", ("f32", "bf16"),
+                          "colour-image-shaped single sample; base of the D sweep 2048..20480"),
 }
+
+# D values of the single-sample bandwidth sweep (bench.py --sweep-d)
+D_SWEEP = (2048, 4096, 8192, 10240, 16384, 20480)
 
 
 def _generators(seed: int):

@@ -107,6 +107,19 @@ def test_colour_workload_sampled(hd, name, dtype):
     assert rep["ok"], rep
 
 
+@pytest.mark.parametrize("D", [hd_inputs.D_SWEEP[0], hd_inputs.D_SWEEP[-1]])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_colour_single_sample_d_sweep_ends(hd, D, dtype):
+    """The single-sample bandwidth sweep (F = 3072, K = 10) at its smallest and largest D."""
+    w = hd_inputs.WORKLOADS["colour_n1"]
+    announce(f"colour_n1 {dtype} D={D}")
+    X, B, C = inputs(w.N, w.F, D, w.K, w.x_dist, dtype=dtype)
+    for packed in (False, True):
+        y, S = run(hd, X, B, C, dtype, packed=packed)
+        rep, _ = check_against_oracle(X, B, C, y, S)
+        assert rep["ok"], (packed, rep)
+
+
 # --- wide features: the X tile streamed through LDS in chunks ---------------
 
 # (N, F, D, K, dtype, kernel): bf16 with F % 8 == 0 double-buffers the chunks
