@@ -80,6 +80,16 @@ def test_infer_argument_errors(L):
     assert _infer(L, N=0, X=None, labels=None, ws=None, wsb=0) == hd.HD_OK
 
 
+def test_large_batch_limits(L):
+    """N > 64 takes the large-batch path: K <= 128, F <= 2^20, tiled B below 2 GiB.
+    These are rejected on the host before any device call."""
+    assert _infer(L, N=100, K=129) == hd.HD_ERR_UNSUPPORTED
+    assert _infer(L, N=100, K=129, dt=hd.HD_BF16) == hd.HD_ERR_UNSUPPORTED
+    assert _infer(L, N=100, F=(1 << 20) + 1, D=64) == hd.HD_ERR_UNSUPPORTED
+    # fp32: 2 * ceil(D/64) * ceil(F/8) KiB >= 2 GiB
+    assert _infer(L, N=100, F=8192, D=64 * 1024) == hd.HD_ERR_UNSUPPORTED
+
+
 def test_other_entry_argument_errors(L):
     assert L.hd_encode(None, FAKE, FAKE, 4, 8, 16, 0, 0, None) == hd.HD_ERR_ARG
     assert L.hd_encode(FAKE, FAKE, FAKE, 4, 0, 16, 0, 0, None) == hd.HD_ERR_ARG
