@@ -880,6 +880,15 @@ __device__ __forceinline__ void lds_reads_complete(uint4 (&v)[NT]) {
 // ---------------------------------------------------------------------------
 constexpr int kDmaFsc = 16;
 
+// Sample tiles per workgroup of the double-buffered kernel, and units per
+// wave per pass over the X chunks: two units with one class block (the X
+// chunks are re-read half as often, at the accumulator count of 128 samples
+// and one unit).
+constexpr int kDmaNtiles = 2;
+__host__ __device__ constexpr int dma_units_per_wave(int ntiles, int kb) {
+  return ntiles == 2 && kb == 1 ? 2 : 1;
+}
+
 __host__ __device__ constexpr int dma_loads_per_wave(int ntiles) {
   return (32 * ntiles * (2 * kDmaFsc + 1) + kThreads - 1) / kThreads;
 }
@@ -891,14 +900,15 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
     int DS, void* __restrict__ workspace) {
   typedef TrBF16 Tr;
   constexpr int NT = 32 * NTILES;
-  constexpr int kPF = prefetch_of(NTILES, KB);
+  constexpr int UPW = dma_units_per_wave(NTILES, KB);  // units per wave per X pass
+  constexpr int kPF = UPW > 1 ? 4 : prefetch_of(NTILES, KB);
   constexpr int FSC = kDmaFsc;
   constexpr int W = 2 * FSC + 1;                 // slots per LDS row
   constexpr int pitch = 8 * W;                   // elements
   constexpr int P = dma_loads_per_wave(NTILES);  // LDS loads per wave per chunk
   constexpr int kDmaSteps = (P + 1) / 2;         // the first steps issue them, two each
-  constexpr int kAfter = 2 * (FSC - kDmaSteps);  // ring loads issued after the last one
-  constexpr int kWait = kAfter < 2 * kPF ? kAfter : 2 * kPF;
+  constexpr int kAfter = 2 * UPW * (FSC - kDmaSteps);  // ring loads issued after the last one
+  constexpr int kWait = kAfter < 2 * UPW * kPF ? kAfter : 2 * UPW * kPF;
   constexpr int buf_elems = P * kThreads * 8;
   static_assert(FSC % kPF == 0 && kDmaSteps <= FSC && kWait <= 63, "chunk schedule");
   // s_waitcnt immediate: vmcnt(kWait), expcnt and lgkmcnt not waited on
@@ -959,37 +969,43 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
                                          brsrc, ((2 * uu + b) * nfs + fs) * 1024 + lane * 16, 0, 0));
   };
-  // this wave's unit in iteration it (a valid unit when it has none: computed, discarded)
-  auto unit_of = [&](int it) {
-    const int u = u_begin + wave + it * kWaves;
+  // this wave's j-th unit in iteration it (a valid unit when it has none: computed, discarded)
+  auto unit_idx = [&](int it, int j) { return u_begin + wave + (it * UPW + j) * kWaves; };
+  auto unit_of = [&](int it, int j) {
+    const int u = unit_idx(it, j);
     return u < u_end ? u : u_begin;
   };
 
   for (int p = 0; p < P; ++p) dma(0, p, 0);
-  // ring slot g % kPF holds f-step g of the current unit
-  uint4 afr[kPF][2];
-  {
-    const int u0 = unit_of(0);
+  // ring slot g % kPF of unit j holds f-step g of the current unit j
+  uint4 afr[UPW][kPF][2];
+#pragma unroll
+  for (int j = 0; j < UPW; ++j) {
+    const int u0 = unit_of(0, j);
 #pragma unroll
     for (int i = 0; i < kPF; ++i) {
-      afr[i][0] = bfrag(u0, i < nfs ? i : nfs - 1, 0);
-      afr[i][1] = bfrag(u0, i < nfs ? i : nfs - 1, 1);
+      afr[j][i][0] = bfrag(u0, i < nfs ? i : nfs - 1, 0);
+      afr[j][i][1] = bfrag(u0, i < nfs ? i : nfs - 1, 1);
     }
   }
   int cur = 0;
-  const int n_it = (u_end - u_begin + kWaves - 1) / kWaves;
+  const int n_it = (u_end - u_begin + kWaves * UPW - 1) / (kWaves * UPW);
   for (int it = 0; it < n_it; ++it) {
-    const bool valid = u_begin + wave + it * kWaves < u_end;
-    const int uu = unit_of(it), un = unit_of(it + 1);
-    CFrags<Tr, KB> cf;
-    cf.load(Cp, 2 * uu, lane);
-    f32x16 vacc[2][NTILES];
+    int uu[UPW], un[UPW];
+    CFrags<Tr, KB> cf[UPW];
+    f32x16 vacc[UPW][2][NTILES];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int j = 0; j < UPW; ++j) {
+      uu[j] = unit_of(it, j);
+      un[j] = unit_of(it + 1, j);
+      cf[j].load(Cp, 2 * uu[j], lane);
 #pragma unroll
-      for (int t = 0; t < NTILES; ++t)
+      for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) vacc[b][t][r] = 0.0f;
+        for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) vacc[j][b][t][r] = 0.0f;
+    }
 
     for (int ch = 0; ch < nchunks; ++ch) {
       const int fs0 = ch * FSC;
@@ -1015,21 +1031,27 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
           xfr[(s + 1) & 1][t] =
               lds_read16_issue(s + 1 < fsn ? xc + t * 64 * pitch + (s + 1) * 32 : xz);
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int j = 0; j < UPW; ++j)
 #pragma unroll
-          for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[s & 1][t]);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES, 0);
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int t = 0; t < NTILES; ++t)
+              Tr::stage1(vacc[j][b][t], afr[j][i][b], xfr[s & 1][t]);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES * UPW, 0);
         if (s < kDmaSteps)
-          __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 2 * UPW + 2, 0);
         else
-          __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 2 * UPW, 0);
         // refill: f-step g of this unit, else the next unit's first steps
         const int g = fs0 + s + kPF;
-        const int ru = g < nfl ? uu : un;
         const int rg0 = g < nfl ? g : g - nfl;
         const int rg = rg0 < nfs ? rg0 : nfs - 1;
-        afr[i][0] = bfrag(ru, rg, 0);
-        afr[i][1] = bfrag(ru, rg, 1);
+#pragma unroll
+        for (int j = 0; j < UPW; ++j) {
+          const int ru = g < nfl ? uu[j] : un[j];
+          afr[j][i][0] = bfrag(ru, rg, 0);
+          afr[j][i][1] = bfrag(ru, rg, 1);
+        }
         if (s < kDmaSteps) {
           dma(nch, 2 * s < P ? 2 * s : P - 1, nbuf);  // a repeated load is harmless
           dma(nch, 2 * s + 1 < P ? 2 * s + 1 : P - 1, nbuf);
@@ -1038,11 +1060,14 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
       lds_reads_complete<NTILES>(xfr[FSC & 1]);  // the padding read of the last step
       cur = nbuf;
     }
-    if (valid) {
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
+    for (int j = 0; j < UPW; ++j) {
+      if (unit_idx(it, j) < u_end) {
 #pragma unroll
-        for (int t = 0; t < NTILES; ++t) cf.template apply<ACT>(vacc[b][t], b, sacc[t]);
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int t = 0; t < NTILES; ++t) cf[j].template apply<ACT>(vacc[j][b][t], b, sacc[t]);
+      }
     }
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // no load into LDS is still in flight
@@ -1098,11 +1123,14 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) 
     c.lds = xbytes > rbytes ? xbytes : rbytes;
     if (Tr::kEsz == 2 && F % 8 == 0 && x16) {
       // two buffers of P * kThreads slots of 16 bytes, plus the zero slot
-      const size_t dbytes = (size_t)2 * dma_loads_per_wave(nt) * kThreads * 16 + 16;
-      if (dbytes <= (size_t)kLdsBytes) {
+      const int dnt = kDmaNtiles;
+      const size_t drbytes = (size_t)kWaves * 32 * dnt * 32 * kbr * 4;
+      const size_t dbytes = (size_t)2 * dma_loads_per_wave(dnt) * kThreads * 16 + 16;
+      if (dbytes <= (size_t)kLdsBytes && drbytes <= (size_t)kLdsBytes) {
         c.dma = true;
+        c.ntiles_per_wg = dnt;
         c.fsc = kDmaFsc;
-        c.lds = dbytes > rbytes ? dbytes : rbytes;
+        c.lds = dbytes > drbytes ? dbytes : drbytes;
       }
     }
   }
@@ -1123,20 +1151,20 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
                       void* ws, hipStream_t stream) {
   const dim3 grid((unsigned)(c.ntiles * c.ds)), block(kThreads);
   if (c.fsc > 0) {
-    if constexpr (NTILES == chunk_ntiles<Tr>(KB)) {
-      if (c.dma) {
-        if constexpr (Tr::kEsz == 2) {
-          static const hipError_t dattr = hipFuncSetAttribute(
-              reinterpret_cast<const void*>(&large_chunked_dma_kernel<NTILES, KB, ACT>),
-              hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
-          if (dattr != hipSuccess) return dattr;
-          hipLaunchKernelGGL((large_chunked_dma_kernel<NTILES, KB, ACT>), grid, block, c.lds,
-                             stream, (const bf16raw*)X, Bp, Cp, labels, scores, (int)N, (int)F,
-                             (int)K, ndb, c.ds, ws);
-          return hipGetLastError();
-        }
-        return hipErrorInvalidValue;
+    if (c.dma) {
+      if constexpr (Tr::kEsz == 2 && NTILES == kDmaNtiles) {
+        static const hipError_t dattr = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&large_chunked_dma_kernel<NTILES, KB, ACT>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+        if (dattr != hipSuccess) return dattr;
+        hipLaunchKernelGGL((large_chunked_dma_kernel<NTILES, KB, ACT>), grid, block, c.lds,
+                           stream, (const bf16raw*)X, Bp, Cp, labels, scores, (int)N, (int)F,
+                           (int)K, ndb, c.ds, ws);
+        return hipGetLastError();
       }
+      return hipErrorInvalidValue;
+    }
+    if constexpr (NTILES == chunk_ntiles<Tr>(KB)) {
       static const hipError_t cattr = hipFuncSetAttribute(
           reinterpret_cast<const void*>(&large_chunked_kernel<Tr, NTILES, KB, ACT>),
           hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
