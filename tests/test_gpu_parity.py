@@ -93,7 +93,7 @@ def test_speech_workload_sampled(hd):
 
 
 @pytest.mark.parametrize("name,dtype", [("colour_k10", "bf16"), ("colour_k100", "bf16"),
-                                        ("colour_k10", "f32")])
+                                        ("colour_k10", "f32"), ("colour_k100", "f32")])
 def test_colour_workload_sampled(hd, name, dtype):
     torch = torch_or_skip()
     w = hd_inputs.WORKLOADS[name]
@@ -128,7 +128,8 @@ CHUNKED = [(200, 3000, 300, 10, "bf16", "dma"), (130, 2999, 200, 7, "bf16", ""),
            (70, 2600, 130, 100, "bf16", "dma"), (150, 1300, 256, 5, "f32", ""),
            (90, 1283, 200, 40, "f32", ""), (65, 1500, 100, 70, "f32", ""),
            (257, 5000, 640, 3, "bf16", "dma"), (129, 2560, 64, 33, "bf16", "dma"),
-           (300, 2568, 1000, 2, "bf16", "dma"), (66, 2602, 200, 50, "bf16", "")]
+           (300, 2568, 1000, 2, "bf16", "dma"), (66, 2602, 200, 50, "bf16", ""),
+           (100, 3000, 200, 128, "bf16", "dma"), (97, 1400, 300, 128, "f32", "")]
 
 
 @pytest.mark.parametrize("N,F,D,K,dtype,kind", CHUNKED)
@@ -202,7 +203,7 @@ def test_hardsign_zero_and_argmax_ties(hd, N):
 
 EDGE = [(1, 1, 1, 1), (2, 2, 7, 2), (3, 5, 33, 1), (31, 17, 2047, 2), (33, 64, 10000, 6),
         (63, 1, 96, 3), (64, 561, 2048, 6), (65, 31, 100, 17), (100, 33, 1000, 33),
-        (129, 200, 640, 100), (300, 16, 64, 64), (1000, 7, 129, 9)]
+        (129, 200, 640, 100), (300, 16, 64, 64), (1000, 7, 129, 9), (65, 300, 200, 128)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
