@@ -65,7 +65,7 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design "
+        print(json.dumps({"error": "this benchmark runs on one GPU; multi-GPU sharding is a design "
                                    "note only (split-N replicas or split-D with an all-reduce of "
                                    "partial scores)", "n_gpus": args.gpus}))
         sys.exit(2)
