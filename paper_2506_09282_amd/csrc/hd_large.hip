@@ -17,7 +17,9 @@
 // sweeps its slice of D. B and C are read from a tiled copy made once per
 // model (the parameter tiling of Sec. III-D): every MFMA A-fragment is one
 // contiguous, fully coalesced 1 KiB block, so B streams straight from L2 into
-// registers with a software-pipelined prefetch ring.
+// registers with a software-pipelined prefetch ring. When even 32 rows of X do
+// not fit LDS (wide F), the F-chunked kernels below stream the tile through
+// LDS in chunks of f-steps instead and keep V in registers across the chunks.
 //
 // Work split. Each of the 4 waves owns "units" of 64 hypervector dimensions
 // (two 32-row MFMA tiles) round-robin within the workgroup's D slice and keeps
@@ -880,10 +882,10 @@ __device__ __forceinline__ void lds_reads_complete(uint4 (&v)[NT]) {
 // ---------------------------------------------------------------------------
 constexpr int kDmaFsc = 16;
 
-// Sample tiles per workgroup of the double-buffered kernel, and units per
-// wave per pass over the X chunks: two units with one class block (the X
-// chunks are re-read half as often, at the accumulator count of 128 samples
-// and one unit).
+// The double-buffered kernel works on 64-sample workgroup tiles. With one
+// class block each wave takes two units per pass over the X chunks: the same
+// accumulator registers as 128 samples times one unit, with the X chunks
+// re-read half as often.
 constexpr int kDmaNtiles = 2;
 __host__ __device__ constexpr int dma_units_per_wave(int ntiles, int kb) {
   return ntiles == 2 && kb == 1 ? 2 : 1;
