@@ -27,6 +27,8 @@
 // When there are too few sample tiles to fill the GPU, D is also split into
 // DS slices whose partial scores are combined by the last-arriving workgroup
 // of each sample tile (ticket counter, self-cleaning).
+#include <type_traits>
+
 #include "hd_common.hpp"
 #include "hd_internal.hpp"
 
@@ -67,6 +69,11 @@ struct TrBF16 {
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast<bf16x8>(a), bitcast<bf16x8>(b), acc,
                                                   0, 0, 0);
   }
+  // first step of a sum: the instruction's accumulator input is the constant 0
+  __device__ static void stage1_init(f32x16& acc, const uint4& a, const uint4& b) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bitcast<bf16x8>(a), bitcast<bf16x8>(b),
+                                                  f32x16{}, 0, 0, 0);
+  }
 };
 
 struct TrF32 {
@@ -86,6 +93,13 @@ struct TrF32 {
   __device__ static void stage1(f32x16& acc, const uint4& a, const uint4& b) {
     const float4 af = bitcast<float4>(a), bf = bitcast<float4>(b);
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.x, bf.x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.y, bf.y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.z, bf.z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.w, bf.w, acc, 0, 0, 0);
+  }
+  __device__ static void stage1_init(f32x16& acc, const uint4& a, const uint4& b) {
+    const float4 af = bitcast<float4>(a), bf = bitcast<float4>(b);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.x, bf.x, f32x16{}, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.y, bf.y, acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.z, bf.z, acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af.w, bf.w, acc, 0, 0, 0);
@@ -576,13 +590,19 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     const bool has_next = un < u_end;
     CFrags<Tr, KB> cf;
     cf.load(Cp, 2 * u, lane);
+    // With 64-sample tiles the unit's first step starts the accumulators from
+    // the matrix instruction's constant-zero input (measured faster there);
+    // with 128-sample tiles they are zeroed here (measured faster there).
+    constexpr bool kZeroInput = NTILES <= 2;
     f32x16 vacc[2][NTILES];
+    if constexpr (!kZeroInput) {
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+      for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int t = 0; t < NTILES; ++t)
+        for (int t = 0; t < NTILES; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) vacc[b][t][r] = 0.0f;
+          for (int r = 0; r < 16; ++r) vacc[b][t][r] = 0.0f;
+    }
 
     uint4 xfr[2][NTILES];
 #pragma unroll
@@ -594,11 +614,11 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     // interleave the refill arithmetic with the matrix instructions and track
     // the wait counters across the loop. Padding steps past nfs (up to
     // kPrefetch-1 of them) multiply a valid, finite B fragment by the zero
-    // slot. The loop is a do-while (it always runs, nfsl >= kPrefetch): with
-    // a possible zero-trip path the compiler would make Stage II wait for
-    // every ring load in flight before using the C fragments loaded above.
-    int fs0 = 0;
-    do {
+    // slot. The unit's first group of kPrefetch steps always runs and issues
+    // ring loads after the C fragment loads above, so Stage II never waits
+    // for the ring in flight before using them (with a zero-trip path the
+    // compiler would make it wait for every ring load).
+    auto steps = [&](int fs0, auto first) __attribute__((always_inline)) {
 #pragma unroll
       for (int i = 0; i < kPrefetch; ++i) {
         const int fs = fs0 + i;
@@ -610,7 +630,12 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
-          for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
+          for (int t = 0; t < NTILES; ++t) {
+            if (kZeroInput && decltype(first)::value && i == 0)
+              Tr::stage1_init(vacc[b][t], afr[i][b], xfr[i & 1][t]);
+            else
+              Tr::stage1(vacc[b][t], afr[i][b], xfr[i & 1][t]);
+          }
         // instruction order per step: the next step's X reads (LDS) first, so
         // they complete under this step's matrix instructions, then the
         // matrix instructions, then the ring refill loads
@@ -628,8 +653,17 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
         afr[i][0] = bfrag(tu, tf, 0);
         afr[i][1] = bfrag(tu, tf, 1);
       }
-      fs0 += kPrefetch;
-    } while (fs0 < nfsl);
+    };
+    if constexpr (kZeroInput) {
+      steps(0, std::true_type{});
+      for (int fs0 = kPrefetch; fs0 < nfsl; fs0 += kPrefetch) steps(fs0, std::false_type{});
+    } else {
+      int fs0 = 0;
+      do {  // always runs at least once (nfsl >= kPrefetch)
+        steps(fs0, std::false_type{});
+        fs0 += kPrefetch;
+      } while (fs0 < nfsl);
+    }
     // Stage II on the finished unit.
 #pragma unroll
     for (int b = 0; b < 2; ++b)
