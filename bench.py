@@ -9,6 +9,7 @@ and the CPU oracle's throughput on a bounded sample as a baseline.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
     python bench.py --sweep-d     # N = 1, F = 3072, K = 10: one line per D (bandwidth map)
+    python bench.py --sweep-n     # F = 561, D = 10240, K = 6: one line per N (samples/s curve)
 """
 from __future__ import annotations
 
@@ -53,6 +54,9 @@ def parse():
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--d", type=int, default=0, help="override the workload's D")
+    p.add_argument("--sweep-n", action="store_true",
+                   help="samples/s curve: one JSON line per N in hd_inputs.N_SWEEP for the "
+                        "activity shape (F=561, D=10240, K=6), no CPU baseline")
     p.add_argument("--sweep-d", action="store_true",
                    help="single-sample bandwidth map: one JSON line per D in hd_inputs.D_SWEEP "
                         "for the colour_n1 shape (F=3072, K=10), no CPU baseline")
@@ -69,6 +73,12 @@ def main():
                                    "note only (split-N replicas or split-D with an all-reduce of "
                                    "partial scores)", "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.sweep_n:
+        args.workload, args.no_cpu_baseline = "activity_n32", True
+        base = hd_inputs.WORKLOADS["activity_n32"]
+        for n in hd_inputs.N_SWEEP:
+            run(args, dataclasses.replace(base, name=f"activity_n{n}", N=n))
+        return
     if args.sweep_d:
         args.workload, args.no_cpu_baseline = "colour_n1", True
         base = hd_inputs.WORKLOADS["colour_n1"]

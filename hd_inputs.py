@@ -74,6 +74,9 @@ WORKLOADS = {
 # D values of the single-sample bandwidth sweep (bench.py --sweep-d)
 D_SWEEP = (2048, 4096, 8192, 10240, 16384, 20480)
 
+# batch sizes of the samples/s curve at D = 10240 (bench.py --sweep-n, activity shape)
+N_SWEEP = (1, 2, 4, 8, 16, 32, 64, 65, 128, 256, 1024, 4096, 16384, 65536)
+
 
 def _generators(seed: int):
     ss = np.random.SeedSequence(seed)

@@ -15,11 +15,31 @@ bool enums_ok(int dt, int act) { return (dt == HD_F32 || dt == HD_BF16) && (act 
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-// The split-D small-batch path serves N <= 64 whenever its scratch fits;
-// everything else takes the batch-split matrix-core path.
-bool use_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  return N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt);
+// Path choice. The split-D small-batch path serves small batches whenever its
+// scratch fits, everything else the batch-split matrix-core path, with two
+// exceptions taken from the measured samples/s curves (F = 561, D = 10240):
+// * bf16 above 16 samples: the small-batch kernel for bf16 makes several
+//   passes over B (72 us at N = 32), the matrix-core path about 48 us;
+// * fp32 with 64 < N <= 256: the matrix-core path has only a few sample tiles
+//   (138 us for N = 65..256), while the small path takes about 32 us per 64
+//   samples, so it runs in 64-sample chunks, one after another on the stream,
+//   when its 64-sample plan runs on the matrix cores (not the VALU fallback).
+enum class Route { kSmall, kSmallChunked, kLarge, kNone };
+constexpr int64_t kSmallMaxNBf16 = 16;
+constexpr int64_t kChunkedMaxN = 256;
+
+Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
+  const bool small_ok = N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt);
+  if (small_ok && (dt == HD_F32 || N <= kSmallMaxNBf16)) return Route::kSmall;
+  if (dt == HD_F32 && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
+      hd::small_matrix_core(hd::kSmallMaxN, F, D, K, dt, tiled))
+    return Route::kSmallChunked;
+  if (hd::large_supported(N, F, D, K, dt)) return Route::kLarge;
+  return small_ok ? Route::kSmall : Route::kNone;
 }
+
+// Batch size of each small-path launch for a route.
+int64_t small_n(Route r, int64_t N) { return r == Route::kSmallChunked ? hd::kSmallMaxN : N; }
 
 hd_status from_hip(hipError_t e) { return e == hipSuccess ? HD_OK : HD_ERR_HIP; }
 
@@ -92,13 +112,17 @@ size_t hd_model_packed_bytes(int64_t F, int64_t D, int64_t K, hd_dtype dt) {
 
 size_t hd_infer_packed_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
   if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
-  if (use_small(N, F, D, K, dt)) return hd::small_workspace_bytes(N, F, D, K, dt);
+  const Route r = route(N, F, D, K, dt, true);
+  if (r == Route::kSmall || r == Route::kSmallChunked)
+    return hd::small_workspace_bytes(small_n(r, N), F, D, K, dt);
   return hd::large_workspace_bytes(N, F, D, K, dt);
 }
 
 size_t hd_infer_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
   if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
-  if (use_small(N, F, D, K, dt)) return hd::small_workspace_bytes(N, F, D, K, dt);
+  const Route r = route(N, F, D, K, dt, false);
+  if (r == Route::kSmall || r == Route::kSmallChunked)
+    return hd::small_workspace_bytes(small_n(r, N), F, D, K, dt);
   return align256(hd::large_packed_bytes(F, D, K, dt)) +
          hd::large_workspace_bytes(N, F, D, K, dt);
 }
@@ -130,17 +154,24 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
   if (!aligned(X, es) || !aligned(labels, 4) || !aligned(scores, 4) || !aligned(workspace, 256) ||
       (packed ? !aligned(packed, 256) : (!aligned(B, es) || !aligned(C, es))))
     return HD_ERR_ARG;
-  const bool small = use_small(N, F, D, K, dt);
-  if (!small && !hd::large_supported(N, F, D, K, dt)) return HD_ERR_UNSUPPORTED;
+  const Route r = route(N, F, D, K, dt, packed != nullptr);
+  if (r == Route::kNone) return HD_ERR_UNSUPPORTED;
   const size_t need = packed ? hd_infer_packed_workspace_bytes(N, F, D, K, dt)
                              : hd_infer_workspace_bytes(N, F, D, K, dt);
   if (need > 0 && !workspace) return HD_ERR_ARG;
   if (workspace_bytes < need) return HD_ERR_WORKSPACE;
 
-  if (small) {
+  if (r == Route::kSmall || r == Route::kSmallChunked) {
     if (packed) B = static_cast<const char*>(packed) + image_layout(F, D, K, dt).large;
-    return from_hip(hd::launch_small(X, B, C, packed != nullptr, labels, scores, N, F, D, K, dt,
-                                     act, workspace, stream));
+    const int64_t step = small_n(r, N);
+    for (int64_t n0 = 0; n0 < N; n0 += step) {
+      const int64_t n = N - n0 < step ? N - n0 : step;
+      const hipError_t e = hd::launch_small(
+          static_cast<const char*>(X) + n0 * F * (int64_t)es, B, C, packed != nullptr,
+          labels + n0, scores ? scores + n0 * K : nullptr, n, F, D, K, dt, act, workspace, stream);
+      if (e != hipSuccess) return HD_ERR_HIP;
+    }
+    return HD_OK;
   }
   void* large_ws = workspace;
   if (!packed) {
@@ -163,8 +194,10 @@ hd_status hd_infer(const void* X, const void* B, const void* C, int32_t* labels,
 
 const char* hd_infer_kernel(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, int packed) {
   if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return "";
-  if (use_small(N, F, D, K, dt)) return hd::small_kernel_name(N, F, D, K, dt, packed != 0);
-  return hd::large_kernel_name(N, F, D, K, dt);
+  const Route r = route(N, F, D, K, dt, packed != 0);
+  if (r == Route::kSmall || r == Route::kSmallChunked)
+    return hd::small_kernel_name(small_n(r, N), F, D, K, dt, packed != 0);
+  return r == Route::kLarge ? hd::large_kernel_name(N, F, D, K, dt) : "";
 }
 
 hd_status hd_infer_packed(const void* X, const void* packed, int32_t* labels, float* scores,

@@ -14,6 +14,9 @@ constexpr int kSmallReplicas = 32;  // replicated score accumulators
 bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 // Name of the kernel launch_small would use for 16-byte aligned operands.
+// Whether the small-batch plan for these sizes (16-byte aligned operands)
+// runs on the matrix cores rather than the VALU fallback.
+bool small_matrix_core(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled);
 const char* small_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled);
 
 // Bytes of the column-tiled model section the small-batch path reads from a

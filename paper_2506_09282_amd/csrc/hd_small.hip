@@ -39,11 +39,16 @@ namespace {
 
 // The VALU kernel serves every layout and alignment; it is the support
 // criterion. Returns nb == 0 when nb * K does not fit in LDS.
-SmallPlan plan_valu(int64_t N, int64_t F, int64_t D, int64_t K) {
+// Samples per pass of the VALU kernel: its X values and accumulators live in
+// registers (kRpt*NB + 4*NB floats per thread), so larger batches take several
+// passes. Beyond 8 (2 with scalar raw loads) the kernel spills to scratch and
+// runs up to two orders of magnitude slower.
+SmallPlan plan_valu(int64_t N, int64_t F, int64_t D, int64_t K, int max_nb) {
   SmallPlan p{};
   p.nblocks = (int)cdiv(D, kW);
   p.grid = p.nblocks < num_cus() ? p.nblocks : num_cus();
-  const int nb = N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : N <= 8 ? 8 : N <= 16 ? 16 : 32;
+  int nb = N <= 1 ? 1 : N <= 2 ? 2 : N <= 4 ? 4 : 8;
+  nb = nb < max_nb ? nb : max_nb;
   const int64_t fixed =
       (int64_t)sizeof(float) * (kWaves * 4 * nb * kW + nb * (kW + 1) + nb * K);
   if (fixed > kLdsBudget) return p;
@@ -82,8 +87,9 @@ size_t frag_bytes(int64_t F, int64_t D, int dt) {
 // with unaligned bases or D % 4 != 0 (kRawScalar) and everything else take
 // the VALU kernel.
 SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay, bool x_aligned) {
-  SmallPlan v = plan_valu(N, F, D, K);
-  if (v.nb == 0 || lay == kRawScalar) return v;
+  if (lay == kRawScalar) return plan_valu(N, F, D, K, 2);
+  SmallPlan v = plan_valu(N, F, D, K, 8);
+  if (v.nb == 0) return v;
   SmallPlan p{};
   p.nblocks = v.nblocks;
   if (lay == kTiled && dt == 0 && x_aligned && N > 8 && frag_ms(F) > 0) {
@@ -193,11 +199,16 @@ hipError_t pack_small_t(const void* B, const void* C, int64_t F, int64_t D, int6
 }  // namespace
 
 bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  return plan_valu(N, F, D, K).nb > 0;
+  return plan_valu(N, F, D, K, 8).nb > 0;
 }
 
 size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   return (size_t)kLine * (1 + kGroups) + sizeof(float) * (size_t)kSmallReplicas * N * K;
+}
+
+bool small_matrix_core(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
+  const SmallPlan p = plan_small(N, F, D, K, dt, tiled ? kTiled : kRawVec, true);
+  return p.nb > 0 && (p.frag || p.bmfma || p.mfma);
 }
 
 const char* small_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {

@@ -162,13 +162,15 @@ hipError_t launch_valu(const SmallPlan& p, const Args& a) {
 
 template <typename T, int LAY>
 hipError_t launch_valu_nb(const SmallPlan& p, const Args& a) {
-  switch (p.nb) {
-    case 1: return launch_valu<T, 1, LAY>(p, a);
-    case 2: return launch_valu<T, 2, LAY>(p, a);
-    case 4: return launch_valu<T, 4, LAY>(p, a);
-    case 8: return launch_valu<T, 8, LAY>(p, a);
-    case 16: return launch_valu<T, 16, LAY>(p, a);
-    default: return launch_valu<T, 32, LAY>(p, a);
+  if constexpr (LAY == kRawScalar) {  // at most 2 samples per pass (register budget)
+    return p.nb == 1 ? launch_valu<T, 1, LAY>(p, a) : launch_valu<T, 2, LAY>(p, a);
+  } else {
+    switch (p.nb) {
+      case 1: return launch_valu<T, 1, LAY>(p, a);
+      case 2: return launch_valu<T, 2, LAY>(p, a);
+      case 4: return launch_valu<T, 4, LAY>(p, a);
+      default: return launch_valu<T, 8, LAY>(p, a);
+    }
   }
 }
 

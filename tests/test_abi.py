@@ -81,13 +81,13 @@ def test_infer_argument_errors(L):
 
 
 def test_large_batch_limits(L):
-    """N > 64 takes the large-batch path: K <= 128, F <= 2^20, tiled B below 2 GiB.
-    These are rejected on the host before any device call."""
-    assert _infer(L, N=100, K=129) == hd.HD_ERR_UNSUPPORTED
+    """N > 256 (fp32) or N > 64 (bf16) takes the large-batch path: K <= 128, F <= 2^20,
+    tiled B below 2 GiB. These are rejected on the host before any device call."""
+    assert _infer(L, N=300, K=129) == hd.HD_ERR_UNSUPPORTED
     assert _infer(L, N=100, K=129, dt=hd.HD_BF16) == hd.HD_ERR_UNSUPPORTED
-    assert _infer(L, N=100, F=(1 << 20) + 1, D=64) == hd.HD_ERR_UNSUPPORTED
+    assert _infer(L, N=300, F=(1 << 20) + 1, D=64) == hd.HD_ERR_UNSUPPORTED
     # fp32: 2 * ceil(D/64) * ceil(F/8) KiB >= 2 GiB
-    assert _infer(L, N=100, F=8192, D=64 * 1024) == hd.HD_ERR_UNSUPPORTED
+    assert _infer(L, N=300, F=8192, D=64 * 1024) == hd.HD_ERR_UNSUPPORTED
 
 
 def test_other_entry_argument_errors(L):

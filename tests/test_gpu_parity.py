@@ -107,6 +107,19 @@ def test_colour_workload_sampled(hd, name, dtype):
     assert rep["ok"], rep
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_activity_shape_largest_batch_sampled(hd, dtype):
+    """The largest N of the samples/s curve (activity shape, N = 65536), sampled rows."""
+    w = hd_inputs.WORKLOADS["activity_n32"]
+    N = hd_inputs.N_SWEEP[-1]
+    announce(f"activity shape {dtype} N={N}")
+    X, B, C = inputs(N, w.F, w.D, w.K, w.x_dist, seed=5, dtype=dtype)
+    y, S = run(hd, X, B, C, dtype, packed=True)
+    rows = np.r_[0:16, 32760:32780, N - 16:N, np.random.default_rng(6).integers(0, N, 32)]
+    rep, _ = check_against_oracle(X, B, C, y, S, rows=rows)
+    assert rep["ok"], rep
+
+
 @pytest.mark.parametrize("D", [hd_inputs.D_SWEEP[0], hd_inputs.D_SWEEP[-1]])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_colour_single_sample_d_sweep_ends(hd, D, dtype):
