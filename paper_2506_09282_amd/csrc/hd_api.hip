@@ -18,14 +18,15 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Path choice. The split-D small-batch path serves small batches whenever its
 // scratch fits, everything else the batch-split matrix-core path, with two
 // exceptions taken from the measured samples/s curves (F = 561, D = 10240):
-// * bf16 above 16 samples: the small-batch kernel for bf16 makes several
-//   passes over B (72 us at N = 32), the matrix-core path about 48 us;
+// * bf16 above 8 samples: the small-batch kernel for bf16 makes several
+//   passes over B (40 us at N = 16, 72 us at N = 32), the matrix-core path
+//   takes 34 us at N = 16..32;
 // * fp32 with 64 < N <= 256: the matrix-core path has only a few sample tiles
 //   (138 us for N = 65..256), while the small path takes about 32 us per 64
 //   samples, so it runs in 64-sample chunks, one after another on the stream,
 //   when its 64-sample plan runs on the matrix cores (not the VALU fallback).
 enum class Route { kSmall, kSmallChunked, kLarge, kNone };
-constexpr int64_t kSmallMaxNBf16 = 16;
+constexpr int64_t kSmallMaxNBf16 = 8;
 constexpr int64_t kChunkedMaxN = 256;
 
 Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
