@@ -29,11 +29,12 @@
  *     the first-maximum convention).
  *   - Limits: 1 <= F, D, K <= 2^30 and 0 <= N <= 2^30; anything larger
  *     returns HD_ERR_UNSUPPORTED. The fused calls on the large-batch path
- *     (N > 64 in bf16; in fp32 N > 256, or N > 64 where the small-batch kernels
- *     would not use the matrix cores) further need K <= 128, F <= 2^20 and a
- *     tiled B below 2 GiB
- *     (2 * ceil(D/64) * ceil(F/s) KiB, s = 16 features for bf16, 8 for fp32);
- *     other sizes also return HD_ERR_UNSUPPORTED.
+ *     (bf16 with N > 8; fp32 with N > 256, or N > 64 where the small-batch
+ *     kernels would not use the matrix cores) further need K <= 128,
+ *     F <= 2^20 and a tiled B below 2 GiB (2 * ceil(D/64) * ceil(F/s) KiB,
+ *     s = 16 features for bf16, 8 for fp32). Otherwise a call with N <= 64
+ *     falls back to the small-batch kernels and a larger one returns
+ *     HD_ERR_UNSUPPORTED.
  *   - Thread safety: the library holds no mutable global state; concurrent
  *     calls are safe when each uses its own workspace.
  */
