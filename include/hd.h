@@ -35,8 +35,10 @@
  *     s = 16 features for bf16, 8 for fp32). Otherwise a call with N <= 64
  *     falls back to the small-batch kernels and a larger one returns
  *     HD_ERR_UNSUPPORTED.
- *   - Thread safety: the library holds no mutable global state; concurrent
- *     calls are safe when each uses its own workspace.
+ *   - Thread safety: besides write-once launch settings kept per device
+ *     (kernel LDS attributes, the compute-unit count), the library holds no
+ *     state between calls; concurrent calls are safe when each uses its own
+ *     workspace.
  */
 #ifndef HD_H_
 #define HD_H_
@@ -90,18 +92,21 @@ size_t hd_infer_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_d
 /*
  * Alg. 1 end to end, fused: labels[N] (and scores[N,K] when non-NULL) from
  * X, B, C, with the encoded matrix H never written to device memory.
- * workspace: caller-owned device buffer of at least
+ * workspace: caller-owned device buffer (256-byte aligned) of at least
  *   hd_infer_workspace_bytes(N, F, D, K, dt) bytes, ZEROED BY THE CALLER
- *   BEFORE ITS FIRST USE. Every call leaves the parts that must start at zero
- *   zeroed again, so a workspace can be reused by consecutive calls on one
- *   stream without clearing. Calls that overlap in time must not share a
- *   workspace. May be NULL only when the required size is 0.
+ *   BEFORE ITS FIRST USE. Every call leaves every byte it used at zero again,
+ *   so one workspace can serve consecutive calls of any shape on one stream
+ *   without clearing, as long as it is large enough for each. Calls that
+ *   overlap in time must not share a workspace. May be NULL only when the
+ *   required size is 0. A call whose launch plan needs more than
+ *   workspace_bytes returns HD_ERR_WORKSPACE and enqueues nothing.
  * The small-batch path splits the hypervector dimension D across workgroups
  * (the paper's small-batch variant, Sec. III-C Alg. 3) and reduces partial
  * scores with fp32 atomics, so score low bits can vary from run to run; the
  * large-batch path splits the batch (the large-batch variant, Alg. 4) and
  * repacks B and C into the workspace first (the parameter tiling of
- * Sec. III-D) unless a packed model is supplied through hd_infer_packed.
+ * Sec. III-D; the copy is cleared again after use) unless a packed model is
+ * supplied through hd_infer_packed.
  */
 hd_status hd_infer(const void *X, const void *B, const void *C, int32_t *labels, float *scores,
                    int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,

@@ -1,5 +1,7 @@
 // C ABI entry points: argument validation on the host (before anything is
 // enqueued), path selection, and kernel launch on the caller's stream.
+#include <atomic>
+
 #include "../../include/hd.h"
 #include "hd_internal.hpp"
 
@@ -67,6 +69,27 @@ bool aligned(const void* p, size_t a) { return (uintptr_t)p % a == 0; }
 
 }  // namespace
 
+namespace hd {
+
+int num_cus() {
+  static std::atomic<int> cus[kMaxDevices];  // 0 until read for that device
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  const bool cached = dev >= 0 && dev < kMaxDevices;
+  if (cached) {
+    const int v = cus[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+  }
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      v <= 0)
+    v = 256;
+  if (cached) cus[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
+
+}  // namespace hd
+
 extern "C" {
 
 const char* hd_status_str(hd_status s) {
@@ -124,8 +147,8 @@ size_t hd_infer_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_d
   const Route r = route(N, F, D, K, dt, false);
   if (r == Route::kSmall || r == Route::kSmallChunked)
     return hd::small_workspace_bytes(small_n(r, N), F, D, K, dt);
-  return align256(hd::large_packed_bytes(F, D, K, dt)) +
-         hd::large_workspace_bytes(N, F, D, K, dt);
+  return align256(hd::large_workspace_bytes(N, F, D, K, dt)) +
+         align256(hd::large_packed_bytes(F, D, K, dt));
 }
 
 hd_status hd_pack_model(const void* B, const void* C, int64_t F, int64_t D, int64_t K, hd_dtype dt,
@@ -174,16 +197,28 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
     }
     return HD_OK;
   }
-  void* large_ws = workspace;
-  if (!packed) {
-    const size_t pb = align256(hd::large_packed_bytes(F, D, K, dt));
-    const hipError_t e = hd::launch_pack(B, C, F, D, K, dt, workspace, stream);
-    if (e != hipSuccess) return HD_ERR_HIP;
-    packed = workspace;
-    large_ws = static_cast<char*>(workspace) + pb;
+  // The plan taken for this X (its alignment can change the tile size and the
+  // D split) must fit the workspace the caller sized with the query.
+  const size_t plan_ws = hd::large_workspace_bytes_for(N, F, D, K, dt, (uintptr_t)X % 16 == 0);
+  if (packed) {
+    if (workspace_bytes < plan_ws) return HD_ERR_WORKSPACE;
+    return from_hip(
+        hd::launch_large(X, packed, labels, scores, N, F, D, K, dt, act, workspace, stream));
   }
-  return from_hip(
-      hd::launch_large(X, packed, labels, scores, N, F, D, K, dt, act, large_ws, stream));
+  // Raw matrices: the scratch that must start at zero (tile counters, split-D
+  // partial scores) stays at offset 0, the same place every route keeps it, and
+  // the packed copy of B and C goes after it. The copy is cleared again once
+  // the kernel has read it, so the whole workspace is zero after the call and
+  // can be reused by a call of any shape.
+  const size_t zone = align256(hd::large_workspace_bytes(N, F, D, K, dt));
+  const size_t pb = hd::large_packed_bytes(F, D, K, dt);
+  if (plan_ws > zone || workspace_bytes < zone + pb) return HD_ERR_WORKSPACE;
+  char* copy = static_cast<char*>(workspace) + zone;
+  if (hd::launch_pack(B, C, F, D, K, dt, copy, stream) != hipSuccess) return HD_ERR_HIP;
+  const hipError_t e =
+      hd::launch_large(X, copy, labels, scores, N, F, D, K, dt, act, workspace, stream);
+  if (e != hipSuccess) return HD_ERR_HIP;
+  return from_hip(hd::launch_zero(copy, pb, stream));
 }
 
 hd_status hd_infer(const void* X, const void* B, const void* C, int32_t* labels, float* scores,

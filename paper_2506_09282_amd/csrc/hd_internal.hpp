@@ -5,7 +5,34 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 namespace hd {
+
+// Launch settings the library takes once per device (kernel attributes, the
+// compute-unit count). They are kept per device id, because a process may
+// drive several GPUs and each call uses whichever device is current; apart
+// from these write-once values the library holds no state between calls.
+constexpr int kMaxDevices = 64;
+
+struct PerDeviceOnce {
+  std::once_flag flag[kMaxDevices];
+  hipError_t err[kMaxDevices] = {};
+};
+
+// Runs f() once for the current device and returns its (remembered) result.
+template <class Fn>
+hipError_t once_per_device(PerDeviceOnce& o, Fn&& f) {
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return f();
+  std::call_once(o.flag[dev], [&] { o.err[dev] = f(); });
+  return o.err[dev];
+}
+
+// Compute units of the current device (256 on MI355X), read once per device.
+int num_cus();
 
 // Small-batch fused path (split-D across workgroups).
 constexpr int kSmallMaxN = 64;
@@ -30,6 +57,10 @@ hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled,
                         float* scores, int64_t N, int64_t F, int64_t D, int64_t K, int dt,
                         int act, void* workspace, hipStream_t stream);
 
+// Zero-fill of a device range (a kernel, not hipMemsetAsync, so that callers
+// may capture it in a graph).
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
+
 // Unfused stages.
 hipError_t launch_encode(const void* X, const void* B, float* H, int64_t N, int64_t F, int64_t D,
                          int dt, int act, hipStream_t stream);
@@ -41,6 +72,9 @@ bool large_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 // Name of the kernel launch_large uses for these sizes ("" if unsupported).
 const char* large_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 size_t large_packed_bytes(int64_t F, int64_t D, int64_t K, int dt);
+// Workspace of the large-batch kernels: for the plan taken with X 16-byte
+// aligned (x16) or not, and the larger of the two (what the size query gives).
+size_t large_workspace_bytes_for(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool x16);
 size_t large_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 hipError_t launch_pack(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,
                        void* packed, hipStream_t stream);

@@ -1180,11 +1180,23 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) 
   // down to slices of 4 units (one per wave): with one sample tile, 64 slices
   // ran bf16 N = 32 at the activity shape in 35 us against 46 us with 16.
   const int64_t units = cdiv(D, 64);
+  const int cus = num_cus();
   int ds = 1;
-  while (c.ntiles * ds < 256 && ds < kMaxSlices && units / (ds * 2) >= kWaves / 2) ds *= 2;
+  while (c.ntiles * ds < cus && ds < kMaxSlices && units / (ds * 2) >= kWaves / 2) ds *= 2;
   c.ds = ds;
   c.ok = true;
   return c;
+}
+
+// Lets kernel k use kLdsBytes of dynamic LDS on the current device (set once
+// per device and kernel).
+template <typename KernelT>
+hipError_t allow_large_lds(KernelT* k) {
+  static PerDeviceOnce once;
+  return once_per_device(once, [k] {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+  });
 }
 
 template <class Tr, int NTILES, int KB, int ACT>
@@ -1195,9 +1207,7 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
   if (c.fsc > 0) {
     if (c.dma) {
       if constexpr (Tr::kEsz == 2 && NTILES == kDmaNtiles) {
-        static const hipError_t dattr = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&large_chunked_dma_kernel<NTILES, KB, ACT>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+        const hipError_t dattr = allow_large_lds(&large_chunked_dma_kernel<NTILES, KB, ACT>);
         if (dattr != hipSuccess) return dattr;
         hipLaunchKernelGGL((large_chunked_dma_kernel<NTILES, KB, ACT>), grid, block, c.lds,
                            stream, (const bf16raw*)X, Bp, Cp, labels, scores, (int)N, (int)F,
@@ -1207,9 +1217,7 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
       return hipErrorInvalidValue;
     }
     if constexpr (NTILES == chunk_ntiles<Tr>(KB)) {
-      static const hipError_t cattr = hipFuncSetAttribute(
-          reinterpret_cast<const void*>(&large_chunked_kernel<Tr, NTILES, KB, ACT>),
-          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+      const hipError_t cattr = allow_large_lds(&large_chunked_kernel<Tr, NTILES, KB, ACT>);
       if (cattr != hipSuccess) return cattr;
       hipLaunchKernelGGL((large_chunked_kernel<Tr, NTILES, KB, ACT>), grid, block, c.lds, stream,
                          (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F,
@@ -1218,9 +1226,7 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
     }
     return hipErrorInvalidValue;
   }
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&large_fused_kernel<Tr, NTILES, KB, ACT>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+  const hipError_t attr = allow_large_lds(&large_fused_kernel<Tr, NTILES, KB, ACT>);
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((large_fused_kernel<Tr, NTILES, KB, ACT>), grid, block, c.lds, stream,
                      (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F, (int)K,
@@ -1280,11 +1286,21 @@ size_t large_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {
   return g.b_bytes + g.c_bytes;
 }
 
-size_t large_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  const LargeCfg c = dt == 0 ? large_cfg<TrF32>(N, F, D, K) : large_cfg<TrBF16>(N, F, D, K);
+size_t large_workspace_bytes_for(int64_t N, int64_t F, int64_t D, int64_t K, int dt,
+                                 bool x16) {
+  const LargeCfg c =
+      dt == 0 ? large_cfg<TrF32>(N, F, D, K, x16) : large_cfg<TrBF16>(N, F, D, K, x16);
   if (!c.ok || c.ds == 1) return 0;
   const size_t cbytes = ((size_t)c.ntiles * sizeof(unsigned) + 255) / 256 * 256;
   return cbytes + sizeof(float) * (size_t)c.ds * N * K;
+}
+
+// The plan (tile size, D slices) depends on whether X is 16-byte aligned, which
+// the size query does not know: size for the larger of the two plans.
+size_t large_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  const size_t a = large_workspace_bytes_for(N, F, D, K, dt, true);
+  const size_t b = large_workspace_bytes_for(N, F, D, K, dt, false);
+  return a > b ? a : b;
 }
 
 hipError_t launch_pack(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,

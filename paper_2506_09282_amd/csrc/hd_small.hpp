@@ -345,18 +345,6 @@ __device__ __forceinline__ void ring3_run(int nitems, Buf& b0, Buf& b1, Buf& b2,
 }
 
 
-inline int num_cus() {
-  static const int cus = [] {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 256;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        v <= 0)
-      return 256;
-    return v;
-  }();
-  return cus;
-}
-
 constexpr int kMfmaSteps[] = {12, 24, 36, 48};  // 4-row steps per wave: F <= 16 * MS
 
 struct SmallPlan {
@@ -381,10 +369,15 @@ inline void widen_for_final(SmallPlan& p, int64_t N, int64_t K) {
   if (p.lds < want && want <= (size_t)kLdsBudget) p.lds = want;
 }
 
+// Lets kernel k use up to kLdsBudget bytes of dynamic LDS on the current
+// device (set once per device and kernel).
 template <typename KernelT>
 hipError_t allow_lds(KernelT* k) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(k),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget);
+  static PerDeviceOnce once;
+  return once_per_device(once, [k] {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget);
+  });
 }
 
 struct Args {

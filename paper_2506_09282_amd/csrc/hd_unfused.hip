@@ -117,6 +117,28 @@ __global__ __launch_bounds__(256) void similarity_kernel(const float* __restrict
   }
 }
 
+// Zero-fill of [p, p + bytes): 16-byte stores over the aligned body, bytes at
+// the ragged end one by one. p is 256-byte aligned (workspace rule).
+__global__ __launch_bounds__(256) void zero_kernel(uint4* __restrict__ p, int64_t n16,
+                                                   unsigned char* __restrict__ tail, int ntail) {
+  const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16;
+       i += (int64_t)gridDim.x * 256)
+    p[i] = z;
+  if (blockIdx.x == 0 && (int)threadIdx.x < ntail) tail[threadIdx.x] = 0;
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return hipSuccess;
+  const int64_t n16 = (int64_t)(bytes / 16);
+  const int ntail = (int)(bytes % 16);
+  const int64_t g = cdiv(n16 > 0 ? n16 : 1, 256);
+  hipLaunchKernelGGL(zero_kernel, dim3((unsigned)(g < 4096 ? g : 4096)), dim3(256), 0, stream,
+                     static_cast<uint4*>(p), n16, static_cast<unsigned char*>(p) + n16 * 16,
+                     ntail);
+  return hipGetLastError();
+}
+
 static int grid_for(int64_t work) {
   const int64_t cap = 1 << 20;
   return (int)(work < cap ? (work > 0 ? work : 1) : cap);

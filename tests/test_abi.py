@@ -110,3 +110,22 @@ def test_product_path_does_not_touch_oracle():
             if f.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in text.lower(), f
+
+
+def test_workspace_query_covers_unaligned_x_plan(L):
+    """The large-batch plan depends on X's alignment: bf16 X that is not
+    16-byte aligned takes the register-staged chunked kernel (128-sample
+    tiles, so fewer tiles and a deeper split of D to fill 256 compute units).
+    The size query must cover that plan's tile counters and split-D partial
+    scores, not only the aligned plan's."""
+    F, D, K = 3072, 10240, 10
+    for N in (8192, 16384):
+        tiles = N // 128
+        ds = 1
+        while tiles * ds < 256:
+            ds *= 2
+        counters = (tiles * 4 + 255) // 256 * 256
+        need = counters + 4 * ds * N * K
+        assert L.hd_infer_packed_workspace_bytes(N, F, D, K, hd.HD_BF16) >= need, N
+        raw = L.hd_infer_workspace_bytes(N, F, D, K, hd.HD_BF16)
+        assert raw >= need + L.hd_model_packed_bytes(F, D, K, hd.HD_BF16) // 2, N
