@@ -1,17 +1,19 @@
 """GPU parity: the HIP path (called through the C ABI) against the oracle.
 
-Scores agree within 1e-4 of ||c_k||_1 plus the fragile-set allowance, labels
-agree except where the oracle's margin lies inside the allowances (see
-tolerance.py); on small-integer inputs every summation order is exact, so
-there scores and labels must be bit-identical.
+Scores agree within 1e-4 of ||c_k||_2 once at most a few HardSign flips on
+dimensions whose encoding sum is within rounding distance of zero are undone,
+and labels agree with the maximum of those scores (see tolerance.py); on
+small-integer inputs every summation order is exact, so there scores and
+labels must be bit-identical.
 """
 import numpy as np
 import pytest
 
 import hd_inputs
 import oracle
-from gpu_util import BF16_DRIFT, RTOL, announce, check_against_oracle, dev, torch_or_skip
-from tolerance import compare
+from gpu_util import (BF16_DRIFT, RTOL, announce, check_against_oracle, check_all_rows, dev,
+                      torch_or_skip)
+from tolerance import compare, drift_scale, score_scale
 
 pytestmark = pytest.mark.gpu
 
@@ -76,24 +78,25 @@ def test_image_workload_sampled(hd, dtype):
     assert rep["ok"], rep
 
 
-def test_speech_workload_sampled(hd):
+def test_speech_workload_all_rows(hd):
+    """Speech shape, bf16, every one of the 65536 rows against the oracle."""
     w = hd_inputs.WORKLOADS["speech"]
-    announce("speech bf16 N=65536")
+    announce("speech bf16 N=65536 (all rows)")
     X, B, C = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype="bf16")
-    y, S = run(hd, X, B, C, "bf16")
-    rows = np.r_[0:32, 4090:4100, w.N - 32:w.N, np.random.default_rng(2).integers(0, w.N, 64)]
-    rep, _ = check_against_oracle(X, B, C, y, S, rows=rows)
+    y, S = run(hd, X, B, C, "bf16", packed=True)
+    rep = check_all_rows(X, B, C, y, S)
+    announce(f"speech all rows: {rep}")
     assert rep["ok"], rep
-    # drift of the bf16 path against the fp32-input oracle
+    # drift of the bf16 path against the fp32-input oracle, sampled rows
+    rows = np.r_[0:32, 4090:4100, w.N - 32:w.N, np.random.default_rng(2).integers(0, w.N, 64)]
     X32, B32, C32 = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype="f32")
     ref32 = oracle.infer(X32, B32, C32, rows=rows)
-    c1 = np.abs(C32.astype(np.float64)).sum(axis=1)
-    drift = np.abs(S[rows] - ref32["S"]) / c1[None, :]
+    drift = np.abs(S[rows] - ref32["S"]) / drift_scale(C32)[None, :]
     assert drift.max() <= BF16_DRIFT, drift.max()
 
 
-@pytest.mark.parametrize("name,dtype", [("colour_k10", "bf16"), ("colour_k100", "bf16"),
-                                        ("colour_k10", "f32"), ("colour_k100", "f32")])
+@pytest.mark.parametrize("name,dtype", [("colour_k10", "bf16"), ("colour_k10", "f32"),
+                                        ("colour_k100", "f32")])
 def test_colour_workload_sampled(hd, name, dtype):
     torch = torch_or_skip()
     w = hd_inputs.WORKLOADS[name]
@@ -104,6 +107,19 @@ def test_colour_workload_sampled(hd, name, dtype):
     y, S = run(hd, X, B, C, dtype, packed=True)
     rows = np.r_[0:24, 8180:8200, w.N - 24:w.N, np.random.default_rng(3).integers(0, w.N, 40)]
     rep, _ = check_against_oracle(X, B, C, y, S, rows=rows)
+    assert rep["ok"], rep
+
+
+def test_colour_k100_all_rows(hd):
+    """Colour shape with 100 classes, bf16, every one of the 16384 rows."""
+    torch = torch_or_skip()
+    w = hd_inputs.WORKLOADS["colour_k100"]
+    assert hd.infer_kernel(w.N, w.F, w.D, w.K, torch.bfloat16) == "large_chunked_dma_kernel"
+    announce("colour_k100 bf16 N=16384 (all rows)")
+    X, B, C = inputs(w.N, w.F, w.D, w.K, w.x_dist, dtype="bf16")
+    y, S = run(hd, X, B, C, "bf16", packed=True)
+    rep = check_all_rows(X, B, C, y, S)
+    announce(f"colour_k100 all rows: {rep}")
     assert rep["ok"], rep
 
 
@@ -184,32 +200,79 @@ def test_wide_features_unaligned_x(hd):
 
 
 # --- exactness on small-integer inputs --------------------------------------
+# Small integers are exact in bf16 and fp32, and every partial sum stays below
+# 2^24, so any summation order is exact: scores and labels must be
+# bit-identical to the oracle's. The cases cover every kernel that serves a
+# benchmark shape, and each asserts which kernel ran.
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("N,F,D,K", [(1, 561, 10240, 6), (32, 33, 1000, 5), (64, 100, 2048, 17),
-                                     (65, 100, 2048, 17), (300, 617, 4096, 26),
-                                     (257, 31, 700, 3)])
-def test_integer_inputs_bit_exact(hd, dtype, N, F, D, K):
-    announce(f"integer {dtype} N={N} F={F} D={D} K={K}")
+INTEGER = [
+    # (N, F, D, K, dtype, packed, kernel)
+    (1, 561, 10240, 6, "f32", False, "small_flat_kernel"),
+    (1, 561, 10240, 6, "f32", True, "small_flat_kernel"),
+    (32, 33, 1000, 5, "f32", False, "small_block_mfma_kernel"),
+    (16, 561, 10240, 6, "f32", True, "small_frag_mfma_kernel"),
+    (32, 561, 10240, 6, "f32", True, "small_frag_mfma_kernel"),
+    (48, 300, 2048, 16, "f32", True, "small_frag_mfma_kernel"),
+    (64, 200, 1000, 12, "f32", True, "small_frag_mfma_kernel"),
+    (64, 561, 4096, 6, "f32", True, "small_mfma_kernel"),
+    (64, 100, 2048, 17, "f32", False, "small_mfma_kernel"),
+    (65, 100, 2048, 17, "f32", False, None),
+    (300, 617, 4096, 26, "f32", False, "large_fused_kernel"),
+    (300, 617, 4096, 26, "bf16", True, "large_fused_kernel"),
+    (257, 31, 700, 3, "bf16", False, "large_fused_kernel"),
+    (32, 561, 2048, 6, "bf16", True, "large_fused_kernel"),
+    (4, 561, 2048, 6, "bf16", True, "small_flat_kernel"),
+    (200, 3072, 1024, 10, "bf16", True, "large_chunked_dma_kernel"),
+    (130, 2600, 512, 100, "bf16", False, "large_chunked_dma_kernel"),
+    (200, 3072, 1024, 10, "f32", True, "large_chunked_kernel"),
+    (150, 2999, 700, 5, "bf16", True, "large_chunked_kernel"),
+]
+
+
+@pytest.mark.parametrize("N,F,D,K,dtype,packed,kernel", INTEGER)
+def test_integer_inputs_bit_exact(hd, N, F, D, K, dtype, packed, kernel):
+    torch = torch_or_skip()
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    if kernel is not None:
+        assert hd.infer_kernel(N, F, D, K, tdt, packed=packed) == kernel
+    announce(f"integer {dtype} N={N} F={F} D={D} K={K} packed={packed} ({kernel})")
     X, B, C = hd_inputs.make_integer_inputs(N, F, D, K, seed=N + F)
-    y, S = run(hd, X, B, C, dtype)
+    y, S = run(hd, X, B, C, dtype, packed=packed)
     ref = oracle.infer(X, B, C)
     assert np.array_equal(S, ref["S"]), np.abs(S - ref["S"]).max()
     assert np.array_equal(y, ref["y"])
 
 
-@pytest.mark.parametrize("N", [5, 200])
-def test_hardsign_zero_and_argmax_ties(hd, N):
-    """Inputs in {-1, 0, 1}: many v = 0 (HardSign ties to +1) and duplicated
-    class rows (argmax ties to the lowest index)."""
-    announce(f"ties N={N}")
-    X, B, C = hd_inputs.make_integer_inputs(N, 40, 512, 4, seed=3, x_range=1, b_range=1)
+# Inputs in {-1, 0, 1}: many v = 0 (HardSign ties to +1, Eq. 1) and duplicated
+# class rows (argmax ties to the lowest index), on every benchmark kernel.
+TIES = [
+    (5, 40, 512, "f32", False, "small_flat_kernel"),
+    (200, 40, 512, "f32", False, "small_mfma_kernel"),
+    (300, 40, 512, "f32", False, "large_fused_kernel"),
+    (5, 40, 512, "bf16", False, "small_flat_kernel"),
+    (200, 40, 512, "bf16", False, "large_fused_kernel"),
+    (32, 40, 512, "f32", True, "small_frag_mfma_kernel"),
+    (64, 200, 1024, "f32", True, "small_frag_mfma_kernel"),
+    (100, 2560, 512, "bf16", True, "large_chunked_dma_kernel"),
+    (100, 2560, 512, "f32", True, "large_chunked_kernel"),
+    (100, 2561, 512, "bf16", False, "large_chunked_kernel"),
+]
+
+
+@pytest.mark.parametrize("N,F,D,dtype,packed,kernel", TIES)
+def test_hardsign_zero_and_argmax_ties(hd, N, F, D, dtype, packed, kernel):
+    torch = torch_or_skip()
+    K = 6
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    assert hd.infer_kernel(N, F, D, K, tdt, packed=packed) == kernel
+    announce(f"ties {dtype} N={N} F={F} D={D} packed={packed} ({kernel})")
+    X, B, C = hd_inputs.make_integer_inputs(N, F, D, 4, seed=3, x_range=1, b_range=1)
     C = np.vstack([C, C[1:2], C[0:1]])
-    for dtype in ("f32", "bf16"):
-        y, S = run(hd, X, B, C, dtype)
-        ref = oracle.infer(X, B, C, want_va=True)
-        assert (ref["V"] == 0).any()
-        assert np.array_equal(S, ref["S"]) and np.array_equal(y, ref["y"])
+    y, S = run(hd, X, B, C, dtype, packed=packed)
+    ref = oracle.infer(X, B, C, want_va=True)
+    assert (ref["V"] == 0).any()
+    assert (ref["S"][:, 4] == ref["S"][:, 1]).all() and (ref["S"][:, 5] == ref["S"][:, 0]).all()
+    assert np.array_equal(S, ref["S"]) and np.array_equal(y, ref["y"])
 
 
 # --- edge shapes --------------------------------------------------------------
@@ -226,6 +289,56 @@ def test_edge_shapes(hd, dtype, N, F, D, K):
     X, B, C = inputs(N, F, D, K, "normal", seed=N * 7 + D, dtype=dtype)
     y, S = run(hd, X, B, C, dtype)
     rep, _ = check_against_oracle(X, B, C, y, S)
+    assert rep["ok"], rep
+
+
+def test_workspace_reused_across_shapes(hd):
+    """One workspace, zeroed once, serves a raw large-batch call (which packs
+    the model into it) and then small-batch calls: every call leaves it zero."""
+    torch = torch_or_skip()
+    F, D, K = 99, 2000, 12
+    shapes = [(1000, "f32"), (4, "f32"), (40, "f32"), (300, "bf16"), (4, "bf16"), (1000, "f32")]
+    need = 0
+    for N, dt in shapes:
+        tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+        need = max(need, hd.infer_workspace_bytes(N, F, D, K, tdt))
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for i, (N, dt) in enumerate(shapes):
+        announce(f"shared workspace N={N} {dt}")
+        X, B, C = inputs(N, F, D, K, seed=20 + i, dtype=dt)
+        y, S = hd.infer(dev(X, dt), dev(B, dt), dev(C, dt), return_scores=True, workspace=ws)
+        torch.cuda.synchronize()
+        rep, _ = check_against_oracle(X, B, C, y.cpu().numpy(), S.cpu().numpy())
+        assert rep["ok"], (N, dt, rep)
+        assert int(ws.count_nonzero()) == 0, (N, dt)
+
+
+def test_unaligned_x_workspace_covers_plan(hd):
+    """bf16 X that is not 16-byte aligned takes the register-staged chunked
+    kernel, whose larger tiles split D more: the size query covers that plan
+    (the bytes just past the workspace stay untouched) and the result is right."""
+    torch = torch_or_skip()
+    w = hd_inputs.WORKLOADS["colour_k10"]
+    N, F, D, K = 8192, w.F, w.D, w.K
+    announce(f"unaligned bf16 X N={N} F={F} K={K}")
+    X, B, C = inputs(N, F, D, K, w.x_dist, seed=12, dtype="bf16")
+    Xd = dev(np.concatenate([np.zeros(1, np.float32), X.ravel()]), "bf16")[1:].view(N, F)
+    assert Xd.data_ptr() % 16 != 0
+    model = hd.pack_model(dev(B, "bf16"), dev(C, "bf16"))
+    need = int(hd.lib().hd_infer_packed_workspace_bytes(N, F, D, K, hd.HD_BF16))
+    assert need > 0
+    guard = 1 << 16
+    buf = torch.zeros(need + guard, dtype=torch.uint8, device="cuda")
+    buf[need:] = 0xA5
+    labels = torch.empty(N, dtype=torch.int32, device="cuda")
+    scores = torch.empty((N, K), dtype=torch.float32, device="cuda")
+    hd.infer_packed(Xd, model, out=(labels, scores), workspace=buf[:need])
+    torch.cuda.synchronize()
+    assert bool((buf[need:] == 0xA5).all())
+    assert int(buf[:need].count_nonzero()) == 0
+    rows = np.r_[0:64, N - 64:N, np.random.default_rng(13).integers(0, N, 64)]
+    rep, _ = check_against_oracle(X, B, C, labels.cpu().numpy(),
+                                  scores.cpu().numpy().astype(np.float64), rows=rows)
     assert rep["ok"], rep
 
 
@@ -276,8 +389,7 @@ def test_packed_model_matches_raw(hd, N, dtype):
     else:
         # the small-batch path sums partial scores with fp32 atomics, so the
         # order (and the last bits) can change between calls
-        c1 = np.abs(C.astype(np.float64)).sum(axis=1)
-        assert np.all(np.abs(S0 - S1) <= 1e-6 * c1[None, :])
+        assert np.all(np.abs(S0 - S1) <= RTOL * score_scale(C)[None, :])
 
 
 # Packed model on the small-batch path against the oracle, covering every
@@ -323,8 +435,7 @@ def test_encode_then_similarity(hd, dtype):
     # Stage II alone on the GPU's own H against the oracle's Stage II on it
     Hn = H.cpu().numpy().astype(np.float64)
     r2 = oracle.similarity(Hn, C)
-    c1 = np.abs(C.astype(np.float64)).sum(axis=1)
-    assert np.all(np.abs(S.cpu().numpy() - r2["S"]) <= RTOL * c1[None, :])
+    assert np.all(np.abs(S.cpu().numpy() - r2["S"]) <= RTOL * score_scale(C)[None, :])
     # identity encoding
     Hi = hd.encode(Xd, Bd, act="identity").cpu().numpy()
     ok, bad, _ = encode_allowed_mismatch(Hi, ref, 120, act="identity")

@@ -1,10 +1,16 @@
 """Comparison rules between a GPU result and the oracle.
 
-Scores are compared relative to ||c_k||_1 = sum_d |c_kd|, the natural scale of
-a similarity with a bipolar hypervector (|h_d| = 1, Eq. 5). HardSign (Eq. 1)
-turns any difference in the fp32 summation order of the encoding sum into a
-+-1 flip when v is within rounding distance of zero; such "fragile"
-dimensions are identified from the oracle's float64 v and the scale
+Scores are compared relative to ||c_k||_2 = sqrt(sum_d c_kd^2), the typical
+magnitude of a similarity between a bipolar hypervector (|h_d| = 1) and class
+k (Eq. 5, Eq. 8: with signs that are not aligned with c_k, the D terms
+h_d c_kd add like a random walk). A per-element |s| scale fails where
+s_nk is near 0; the larger ||c_k||_1 scale (the worst case of the sum) lets
+a kernel that drops or double-counts one dimension pass, since one term
+|c_kd| is about ||c_k||_1 / D.
+
+HardSign (Eq. 1) turns any difference in the fp32 summation order of the
+encoding sum into a +-1 flip when v is within rounding distance of zero; such
+"fragile" dimensions are identified from the oracle's float64 v and the scale
 a = sum_f |x_f||b_fd|, and each flip may move a score by 2|c_kd|.
 
 Fragile set:   Fr_n = { d : |v_nd| <= gamma_F * a_nd },
@@ -12,9 +18,20 @@ Fragile set:   Fr_n = { d : |v_nd| <= gamma_F * a_nd },
 (Higham's bound for an F-term dot product, with the unit roundoff doubled
 because the GPU accumulation order and the matrix-core internal rounding are
 unspecified).
-Score allowance: A_nk = rtol * ||c_k||_1 + 2 * sum_{d in Fr_n} |c_kd|.
-Labels: equal, or the oracle's margin between the two labels lies within the
-two allowances (exact ties resolve to the lowest index and must match).
+Scores: a row's difference from the oracle must be explained, for all K
+classes at once, by at most MAX_FLIPS HardSign flips on Fr_n (a flip of
+dimension d moves score k by -2 h_d c_kd), up to rtol * ||c_k||_2.
+Labels: the GPU label must be a maximum of the flip-corrected oracle scores
+within the two classes' tolerances (exact ties resolve to the lowest index
+and must match). With labels alone, the worst-case allowance
+A_nk = rtol * ||c_k||_2 + 2 * sum_{d in Fr_n} |c_kd| bounds the margin.
+
+bf16 drift (the bf16 inputs against the fp32-input oracle) is a property of
+rounding X, B and C to bf16, not of a kernel: even the exact result on the
+rounded inputs drifts by up to about 0.27 ||c_k||_2 at the benchmark shapes
+(HardSign flips where |v| is below the rounding change of v), but by at most
+about 3.4e-3 ||c_k||_1. The 3e-2 drift bound is therefore applied on the
+||c_k||_1 scale (drift_scale), where an exact bf16 computation meets it.
 """
 from __future__ import annotations
 
@@ -27,15 +44,30 @@ def gamma(F: int, u: float = U_FP32_DOUBLED) -> float:
     return F * u / (1.0 - F * u)
 
 
+def score_scale(C):
+    """||c_k||_2 per class: the scale of the relative score tolerance."""
+    C = np.asarray(C, dtype=np.float64)
+    return np.sqrt((C * C).sum(axis=1))
+
+
+def drift_scale(C):
+    """||c_k||_1 per class: the scale of the bf16 drift bound (see above)."""
+    return np.abs(np.asarray(C, dtype=np.float64)).sum(axis=1)
+
+
 def score_allowance(ref, C, F: int, rtol: float, act: str = "hardsign"):
     """Per-(n, k) allowance for |S_gpu - S_oracle|."""
     C = np.asarray(C, dtype=np.float64)
     absC = np.abs(C)
     if act == "hardsign":
+        base = rtol * score_scale(C)[None, :]
+        if "V" not in ref:
+            # no v, a from the oracle: the rule without the fragile-set term,
+            # which is never looser than the full rule
+            return np.broadcast_to(base, ref["S"].shape), None
         fragile = np.abs(ref["V"]) <= gamma(F) * ref["A"]
         fr_mass = fragile.astype(np.float64) @ absC.T
-        c1 = absC.sum(axis=1)
-        return rtol * c1[None, :] + 2.0 * fr_mass, fragile
+        return base + 2.0 * fr_mass, fragile
     # identity: S = V C^T; a perturbation of V bounded by gamma_F*A moves
     # s_nk by at most gamma_F * sum_d A_nd |c_kd|; the second stage adds a
     # relative rtol of sum_d |v_nd||c_kd|.
@@ -44,38 +76,116 @@ def score_allowance(ref, C, F: int, rtol: float, act: str = "hardsign"):
     return prop + rtol * scale, None
 
 
+MAX_FLIPS = 3  # HardSign flips per row that a score difference may be explained by
+
+
+def _explain(r, delta, base, max_flips=MAX_FLIPS):
+    """Smallest set T of candidate flips (rows of delta, each the move of all
+    K scores that one flipped dimension causes) with |r - sum_T delta| <= base
+    for every class; None when no set of at most max_flips does it."""
+    if np.all(np.abs(r) <= base):
+        return ()
+    m = delta.shape[0]
+    if m >= 1:
+        ok = np.all(np.abs(r[None, :] - delta) <= base[None, :], axis=1)
+        if ok.any():
+            return (int(np.flatnonzero(ok)[0]),)
+    if m >= 2 and max_flips >= 2:
+        res = r[None, None, :] - delta[:, None, :] - delta[None, :, :]
+        ok = np.all(np.abs(res) <= base, axis=2) & np.triu(np.ones((m, m), bool), 1)
+        if ok.any():
+            i, j = np.argwhere(ok)[0]
+            return (int(i), int(j))
+    if 3 <= m <= 64 and max_flips >= 3:
+        pair = delta[:, None, :] + delta[None, :, :]
+        upper = np.triu(np.ones((m, m), bool), 1)
+        for i in range(m - 2):
+            res = r[None, None, :] - delta[i][None, None, :] - pair
+            ok = np.all(np.abs(res) <= base, axis=2) & upper
+            ok[: i + 1, :] = False
+            if ok.any():
+                j, k = np.argwhere(ok)[0]
+                return (i, int(j), int(k))
+    return None
+
+
 def compare(S_gpu, y_gpu, ref, C, F: int, rtol: float, act: str = "hardsign",
             S_ref=None):
     """Check GPU scores/labels against oracle output ``ref`` (dict with
-    y, S, V, A in float64). Returns a report dict; ``ok`` is the verdict."""
+    y, S and, for the full rule, V and A in float64). Returns a report dict;
+    ``ok`` is the verdict and ``bad_rows`` lists the rows that fail.
+
+    HardSign scores: each row's difference from the oracle must be within
+    rtol * ||c_k||_2 for every class k after undoing a set of at most
+    MAX_FLIPS HardSign flips on the row's fragile set, the same flips for all
+    classes (a flip of dimension d moves score k by -2 h_d c_kd). Labels:
+    the GPU's label must be a maximum of those flip-corrected oracle scores
+    within the two classes' tolerances. Without scores (labels only) the
+    worst-case allowance of score_allowance decides."""
+    C = np.asarray(C, dtype=np.float64)
     allow, fragile = score_allowance(ref, C, F, rtol, act)
     S_or = ref["S"] if S_ref is None else S_ref
     y_or = ref["y"]
-    rep = {"n": int(len(y_or))}
-    if S_gpu is not None:
-        S_gpu = np.asarray(S_gpu, dtype=np.float64)
-        err = np.abs(S_gpu - S_or)
-        rep["score_ok"] = bool(np.all(err <= allow))
-        rep["score_bad"] = int(np.sum(err > allow))
-        if act == "hardsign":
-            c1 = np.abs(np.asarray(C, dtype=np.float64)).sum(axis=1)
-            rel = err / c1[None, :]
-            rep["max_rel_c1"] = float(rel.max()) if rel.size else 0.0
-            rep["literal_violations"] = int(np.sum(rel > rtol))
-    else:
-        rep["score_ok"] = True
+    R, K = S_or.shape
+    idx = np.arange(R)
+    rep = {"n": int(R)}
     y_gpu = np.asarray(y_gpu).astype(np.int64)
-    idx = np.arange(len(y_or))
-    in_range = (y_gpu >= 0) & (y_gpu < np.asarray(C).shape[0])
+    in_range = (y_gpu >= 0) & (y_gpu < K)
     rep["labels_in_range"] = bool(np.all(in_range))
-    yg = np.clip(y_gpu, 0, np.asarray(C).shape[0] - 1)
-    mism = yg != y_or
-    just = S_or[idx, yg] >= S_or[idx, y_or] - (allow[idx, yg] + allow[idx, y_or])
+    yg = np.clip(y_gpu, 0, K - 1)
+    bad = ~in_range
+    if act != "hardsign":
+        if S_gpu is not None:
+            err = np.abs(np.asarray(S_gpu, dtype=np.float64) - S_or)
+            bad |= (err > allow).any(axis=1)
+            rep["score_bad"] = int(np.sum(err > allow))
+        just = S_or[idx, yg] >= S_or[idx, y_or] - (allow[idx, yg] + allow[idx, y_or])
+        mism = yg != y_or
+        bad |= mism & ~just
+    elif S_gpu is None:
+        # labels only: the worst-case allowance (every fragile dimension flipped)
+        mism = yg != y_or
+        just = S_or[idx, yg] >= S_or[idx, y_or] - (allow[idx, yg] + allow[idx, y_or])
+        bad |= mism & ~just
+    else:
+        S_gpu = np.asarray(S_gpu, dtype=np.float64)
+        base = rtol * score_scale(C)
+        r = S_gpu - S_or
+        rel = np.abs(r) / base[None, :] * rtol
+        rep["max_rel_c2"] = float(rel.max()) if rel.size else 0.0
+        rep["literal_violations"] = int(np.sum(np.abs(r) > base[None, :]))
+        S_exp = S_or.copy()  # oracle scores with the explaining flips applied
+        flips = 0
+        score_bad = np.zeros(R, dtype=bool)
+        H_or = None if fragile is None else np.where(ref["V"] >= 0, 1.0, -1.0)
+        for n in np.flatnonzero((np.abs(r) > base[None, :]).any(axis=1)):
+            T = None
+            if fragile is not None:
+                ds = np.flatnonzero(fragile[n])
+                delta = (-2.0 * H_or[n, ds])[:, None] * C[:, ds].T
+                T = _explain(r[n], delta, base)
+                if T is not None:
+                    S_exp[n] += delta[list(T)].sum(axis=0) if T else 0.0
+                    flips += len(T)
+            if T is None:
+                score_bad[n] = True
+        rep["score_bad"] = int(score_bad.sum())
+        rep["flips"] = flips
+        bad |= score_bad
+        top = S_exp.argmax(axis=1)
+        just = S_exp[idx, yg] >= S_exp[idx, top] - (base[yg] + base[top])
+        mism = yg != y_or
+        bad |= ~just
+    # with scores (HardSign) the label must be near the maximum of the
+    # flip-corrected scores; otherwise only a mismatch needs justifying
+    label_bad = ~just if (act == "hardsign" and S_gpu is not None) else mism & ~just
+    rep["score_ok"] = rep.get("score_bad", 0) == 0
     rep["label_mismatch"] = int(mism.sum())
-    rep["label_unjustified"] = int(np.sum(mism & ~just))
+    rep["label_unjustified"] = int(label_bad.sum())
     if fragile is not None:
         rep["fragile_dims"] = int(fragile.sum())
-    rep["ok"] = bool(rep["score_ok"] and rep["labels_in_range"] and rep["label_unjustified"] == 0)
+    rep["bad_rows"] = np.flatnonzero(bad)
+    rep["ok"] = bool(not bad.any())
     return rep
 
 
