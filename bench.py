@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-floors", action="store_true",
+                   help="skip the streaming-read and empty-launch floor measurements")
     p.add_argument("--d", type=int, default=0, help="override the workload's D")
     p.add_argument("--sweep-n", action="store_true",
                    help="samples/s curve: one JSON line per N in hd_inputs.N_SWEEP for the "
@@ -74,13 +76,13 @@ def main():
                                    "partial scores)", "n_gpus": args.gpus}))
         sys.exit(2)
     if args.sweep_n:
-        args.workload, args.no_cpu_baseline = "activity_n32", True
+        args.workload, args.no_cpu_baseline, args.no_floors = "activity_n32", True, True
         base = hd_inputs.WORKLOADS["activity_n32"]
         for n in hd_inputs.N_SWEEP:
             run(args, dataclasses.replace(base, name=f"activity_n{n}", N=n))
         return
     if args.sweep_d:
-        args.workload, args.no_cpu_baseline = "colour_n1", True
+        args.workload, args.no_cpu_baseline, args.no_floors = "colour_n1", True, True
         base = hd_inputs.WORKLOADS["colour_n1"]
         for d in hd_inputs.D_SWEEP:
             run(args, dataclasses.replace(base, name=f"colour_n1_d{d}", D=d))
@@ -187,7 +189,7 @@ def run(args, w):
     kernel = hd.infer_kernel(w.N, w.F, w.D, w.K, Xd.dtype, packed=True)
     traffic = recorded_traffic(w.name, kernel)
     if small:
-        alg_bytes = esz * (w.N * w.F + w.F * w.D + w.K * w.D) + 4 * w.N
+        alg_bytes = alg_bytes_of(w, dtype)
         roof = {"bound": "hbm", "achieved": alg_bytes / launch_s / 1e9, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "traffic": traffic}
     else:
@@ -209,6 +211,12 @@ def run(args, w):
                    "kernel": kernel, "model": "packed once before timing"},
         "roofline": roof,
     }
+    if not args.no_floors:
+        fl = measure_floors(dev, stream, alg_bytes_of(w, dtype) if small else 0, copies)
+        out["floors"] = fl
+        if small and fl.get("stream_read_GBs"):
+            roof["measured_peak"] = fl["stream_read_GBs"]
+            roof["frac_of_measured"] = round(roof["achieved"] / fl["stream_read_GBs"], 4)
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib << 18  # fp32 elements
         src = torch.ones(n, device=dev)
@@ -219,6 +227,80 @@ def run(args, w):
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, X, B, C, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def alg_bytes_of(w, dtype) -> int:
+    """Algorithmic bytes of one call: X, B and C read once, labels written."""
+    esz = 4 if dtype == "f32" else 2
+    return esz * (w.N * w.F + w.F * w.D + w.K * w.D) + 4 * w.N
+
+
+def measure_floors(dev, stream, same_bytes: int, copies: int):
+    """Floors of the machine the benchmark runs on, from bench_floors.hip:
+    the streaming read bandwidth of a 2 GiB buffer (well past the 256 MB
+    last-level cache), the time of one launch that only reads `same_bytes`
+    bytes (cold: rotated over enough buffers to exceed the cache, replayed in
+    a graph like the timed steps), and the time of one empty launch."""
+    import ctypes
+    import torch
+    lib_path = os.path.join(ROOT, "bench_floors.so")
+    if not os.path.exists(lib_path):
+        from paper_2506_09282_amd import build as hbuild
+        hbuild.build_floors()
+    L = ctypes.CDLL(lib_path)
+    L.floors_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                     ctypes.c_int, ctypes.c_void_p]
+    L.floors_stream_read.restype = ctypes.c_int
+    L.floors_empty.argtypes = [ctypes.c_void_p]
+    L.floors_empty.restype = ctypes.c_int
+    blocks = 4096
+    sink = torch.empty(blocks, dtype=torch.float32, device=dev)
+
+    def ev_time(fn, reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            fn()
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) / reps / 1e3
+
+    def check(rc):
+        if rc != 0:
+            raise RuntimeError(f"bench_floors launch failed ({rc})")
+
+    out = {}
+    big = torch.empty(2 << 30, dtype=torch.uint8, device=dev)
+    n16 = big.numel() // 16
+    sp = stream.cuda_stream
+    t = ev_time(lambda: check(L.floors_stream_read(big.data_ptr(), n16, sink.data_ptr(), blocks,
+                                                   sp)), 5)
+    out["stream_read_GBs"] = round(big.numel() / t / 1e9, 1)
+    del big
+
+    def graph_time(fn, n_per_graph=100, reps=20):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(n_per_graph):
+                fn(i)
+        stream.synchronize()
+        return ev_time(g.replay, reps) / n_per_graph
+
+    out["empty_launch_us"] = round(graph_time(lambda i: check(L.floors_empty(sp))) * 1e6, 3)
+    if same_bytes > 0:
+        nb = max(copies, 1)
+        bufs = [torch.empty(same_bytes // 16 * 16, dtype=torch.uint8, device=dev)
+                for _ in range(nb)]
+        n = bufs[0].numel() // 16
+        t = graph_time(lambda i: check(L.floors_stream_read(
+            bufs[i % nb].data_ptr(), n, sink.data_ptr(), 1024, sp)))
+        out["read_same_bytes_us"] = round(t * 1e6, 3)
+        out["read_same_bytes"] = int(bufs[0].numel())
+        del bufs
+    torch.cuda.synchronize()
+    return out
 
 
 def source_digest() -> str:
@@ -253,8 +335,20 @@ def recorded_traffic(workload: str, kernel: str):
     return None
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, X, B, C, target_s):
-    """The oracle as it stands, on the host cores, over a bounded sample."""
+    """The oracle as it stands, on the host cores, over a bounded sample; then
+    on one thread over a smaller sample."""
     import oracle
     orc = oracle.default()
     threads = orc.threads(0)
@@ -268,10 +362,18 @@ def cpu_baseline(w, X, B, C, target_s):
     t0 = time.perf_counter()
     orc.infer(X, B, C, rows=rows)
     dt = time.perf_counter() - t0
+    # one thread: about a quarter of the time budget
+    n1 = int(max(1, min(target_s / 4 / max(per_row * threads, 1e-9), 1e6)))
+    rows1 = np.arange(n1) % w.N
+    t0 = time.perf_counter()
+    orc.infer(X, B, C, rows=rows1, nthreads=1)
+    dt1 = time.perf_counter() - t0
     return {"value": round(n_rows / dt, 3), "unit": "samples/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "single_thread_value": round(n1 / dt1, 3),
             "sample": f"{n_rows} rows of the same workload (rows cycled over the batch), "
-                      f"float64 loops, {dt:.1f} s"}
+                      f"float64 loops, {dt:.1f} s on {threads} threads; {n1} rows in "
+                      f"{dt1:.1f} s on one thread"}
 
 
 if __name__ == "__main__":

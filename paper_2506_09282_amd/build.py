@@ -59,5 +59,23 @@ def build(verbose: bool = False, jobs: int = 0) -> str:
     return LIB
 
 
+FLOORS_SRC = os.path.join(ROOT, "bench_floors.hip")
+FLOORS_LIB = os.path.join(ROOT, "bench_floors.so")
+
+
+def build_floors(verbose: bool = False) -> str:
+    """The benchmark's measurement-floor kernels (bench_floors.hip, beside
+    bench.py): not part of libhd.so."""
+    tmp = FLOORS_LIB + ".tmp"
+    cmd = [HIPCC, *CFLAGS, "-shared", FLOORS_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {FLOORS_SRC}:\n{r.stdout}{r.stderr}")
+    os.replace(tmp, FLOORS_LIB)
+    return FLOORS_LIB
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
