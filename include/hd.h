@@ -135,6 +135,27 @@ hd_status hd_infer_packed(const void *X, const void *packed, int32_t *labels, fl
                           void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * hd_infer_packed without a caller workspace, for callers that cannot
+ * allocate device memory or pass one in: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation. It allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine); the
+ * scratch its kernels need (tickets, replicated partial scores, split-D
+ * partials) is a fixed device array of hd_noalloc_scratch_bytes() bytes
+ * (4 MiB) inside the library, one per GPU, held until the process ends.
+ * Calls whose scratch need (hd_infer_packed_workspace_bytes) exceeds that
+ * return HD_ERR_WORKSPACE before anything is enqueued. Each call first
+ * clears the part it uses (a fill kernel on `stream`), so the array's
+ * contents from an earlier call do not matter. All calls on one GPU share
+ * the array: calls that overlap in time on one GPU (other streams, other
+ * host threads) race and must be serialised by the caller. Otherwise the
+ * arguments, checks and results are those of hd_infer_packed.
+ */
+size_t hd_noalloc_scratch_bytes(void);
+hd_status hd_infer_packed_noalloc(const void *X, const void *packed, int32_t *labels,
+                                  float *scores, int64_t N, int64_t F, int64_t D, int64_t K,
+                                  hd_dtype dt, hd_act act, hipStream_t stream);
+
+/*
  * Introspection: the name of the main kernel that hd_infer (packed == 0) or
  * hd_infer_packed (packed != 0) launches for these sizes, assuming 16-byte
  * aligned operands; "" when the call would be rejected. The returned string

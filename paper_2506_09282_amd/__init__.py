@@ -32,6 +32,8 @@ SYMBOLS = (
     "hd_infer_packed_workspace_bytes",
     "hd_infer_packed",
     "hd_infer_kernel",
+    "hd_noalloc_scratch_bytes",
+    "hd_infer_packed_noalloc",
 )
 
 _lib = None
@@ -79,6 +81,10 @@ def lib():
         L.hd_infer_packed.restype = i32
         L.hd_infer_kernel.argtypes = [i64, i64, i64, i64, i32, i32]
         L.hd_infer_kernel.restype = ctypes.c_char_p
+        L.hd_noalloc_scratch_bytes.argtypes = []
+        L.hd_noalloc_scratch_bytes.restype = sz
+        L.hd_infer_packed_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, i32, vp]
+        L.hd_infer_packed_noalloc.restype = i32
         _lib = L
         return L
 
@@ -269,4 +275,29 @@ def infer_packed(X, model: PackedModel, act: str = "hardsign", return_scores: bo
                            ACTS[act], ws.data_ptr() if ws is not None else None,
                            ws.numel() if ws is not None else 0, _stream_ptr(X.device))
     _raise(st, "hd_infer_packed")
+    return (labels, scores) if (return_scores or out is not None) else labels
+
+
+def infer_packed_noalloc(X, model: PackedModel, act: str = "hardsign", return_scores: bool = False,
+                         out=None):
+    """``infer_packed`` on the library's fixed scratch (no workspace argument;
+    calls on one GPU must not overlap in time)."""
+    torch = _torch()
+    _check_dev(X)
+    if _dt(X) != model.dt:
+        raise TypeError("X dtype differs from the packed model's")
+    N, F = X.shape
+    if F != model.F:
+        raise ValueError("shape mismatch")
+    D, K, dt = model.D, model.K, model.dt
+    if out is not None:
+        labels, scores = out
+    else:
+        labels = torch.empty(N, dtype=torch.int32, device=X.device)
+        scores = (torch.empty((N, K), dtype=torch.float32, device=X.device)
+                  if return_scores else None)
+    st = lib().hd_infer_packed_noalloc(X.data_ptr(), model.image.data_ptr(), labels.data_ptr(),
+                                       scores.data_ptr() if scores is not None else None, N, F, D,
+                                       K, dt, ACTS[act], _stream_ptr(X.device))
+    _raise(st, "hd_infer_packed_noalloc")
     return (labels, scores) if (return_scores or out is not None) else labels

@@ -166,10 +166,12 @@ hd_status hd_pack_model(const void* B, const void* C, int64_t F, int64_t D, int6
   return HD_OK;
 }
 
+// dry: run every host-side check and return the status the call would have,
+// enqueueing nothing.
 static hd_status infer_common(const void* X, const void* B, const void* C, const void* packed,
                               int32_t* labels, float* scores, int64_t N, int64_t F, int64_t D,
                               int64_t K, hd_dtype dt, hd_act act, void* workspace,
-                              size_t workspace_bytes, hipStream_t stream) {
+                              size_t workspace_bytes, hipStream_t stream, bool dry = false) {
   if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
   if (!dims_ok(N, F, D, K)) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
@@ -186,6 +188,7 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
   if (workspace_bytes < need) return HD_ERR_WORKSPACE;
 
   if (r == Route::kSmall || r == Route::kSmallChunked) {
+    if (dry) return HD_OK;
     if (packed) B = static_cast<const char*>(packed) + image_layout(F, D, K, dt).large;
     const int64_t step = small_n(r, N);
     for (int64_t n0 = 0; n0 < N; n0 += step) {
@@ -202,6 +205,7 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
   const size_t plan_ws = hd::large_workspace_bytes_for(N, F, D, K, dt, (uintptr_t)X % 16 == 0);
   if (packed) {
     if (workspace_bytes < plan_ws) return HD_ERR_WORKSPACE;
+    if (dry) return HD_OK;
     return from_hip(
         hd::launch_large(X, packed, labels, scores, N, F, D, K, dt, act, workspace, stream));
   }
@@ -213,6 +217,7 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
   const size_t zone = align256(hd::large_workspace_bytes(N, F, D, K, dt));
   const size_t pb = hd::large_packed_bytes(F, D, K, dt);
   if (plan_ws > zone || workspace_bytes < zone + pb) return HD_ERR_WORKSPACE;
+  if (dry) return HD_OK;
   char* copy = static_cast<char*>(workspace) + zone;
   if (hd::launch_pack(B, C, F, D, K, dt, copy, stream) != hipSuccess) return HD_ERR_HIP;
   const hipError_t e =
@@ -242,6 +247,67 @@ hd_status hd_infer_packed(const void* X, const void* packed, int32_t* labels, fl
   if (N > 0 && !packed) return HD_ERR_ARG;
   return infer_common(X, nullptr, nullptr, packed, labels, scores, N, F, D, K, dt, act, workspace,
                       workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------------------
+// hd_infer_packed_noalloc: hd_infer_packed with the library's own scratch.
+// The scratch is a file-scope device array: each GPU the library runs on
+// holds one copy for the life of the process. Host code never passes the
+// array's name to a kernel (in host code it is a stand-in, not a device
+// address); it takes the device address once per device with
+// hipGetSymbolAddress and uses that.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kScratchBytes = size_t(4) << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+hd::PerDeviceOnce g_scratch_once;
+void* g_scratch_ptr[hd::kMaxDevices];
+
+hd_status scratch_ptr(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= hd::kMaxDevices) return HD_ERR_HIP;
+  const hipError_t e = hd::once_per_device(g_scratch_once, [dev] {
+    void* p = nullptr;
+    const hipError_t r = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (r == hipSuccess) g_scratch_ptr[dev] = p;
+    return r;
+  });
+  if (e != hipSuccess || !g_scratch_ptr[dev]) return HD_ERR_HIP;
+  *out = g_scratch_ptr[dev];
+  return HD_OK;
+}
+
+}  // namespace
+
+size_t hd_noalloc_scratch_bytes(void) { return kScratchBytes; }
+
+hd_status hd_infer_packed_noalloc(const void* X, const void* packed, int32_t* labels,
+                                  float* scores, int64_t N, int64_t F, int64_t D, int64_t K,
+                                  hd_dtype dt, hd_act act, hipStream_t stream) {
+  if (N > 0 && !packed) return HD_ERR_ARG;
+  if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
+  if (!dims_ok(N, F, D, K)) return HD_ERR_UNSUPPORTED;
+  if (N == 0) return HD_OK;
+  const size_t need = hd_infer_packed_workspace_bytes(N, F, D, K, dt);
+  if (need > kScratchBytes) return HD_ERR_WORKSPACE;
+  void* ws = nullptr;
+  // every check of the allocating entry point, before anything is enqueued
+  // (the scratch's alignment and size stand in for a caller's workspace)
+  hd_status st = infer_common(X, nullptr, nullptr, packed, labels, scores, N, F, D, K, dt, act,
+                              reinterpret_cast<void*>(uintptr_t(256)), kScratchBytes, stream,
+                              true);
+  if (st != HD_OK) return st;
+  st = scratch_ptr(&ws);
+  if (st != HD_OK) return st;
+  // The kernels leave their scratch zeroed, but a call that never finished
+  // (or a caller that wrote the memory) would leave it otherwise: clear the
+  // part this call uses with a fill kernel (not a memset node, so the call
+  // can be captured in a graph).
+  if (need > 0 && hd::launch_zero(ws, need, stream) != hipSuccess) return HD_ERR_HIP;
+  return infer_common(X, nullptr, nullptr, packed, labels, scores, N, F, D, K, dt, act, ws,
+                      kScratchBytes, stream);
 }
 
 }  // extern "C"

@@ -129,3 +129,19 @@ def test_workspace_query_covers_unaligned_x_plan(L):
         assert L.hd_infer_packed_workspace_bytes(N, F, D, K, hd.HD_BF16) >= need, N
         raw = L.hd_infer_workspace_bytes(N, F, D, K, hd.HD_BF16)
         assert raw >= need + L.hd_model_packed_bytes(F, D, K, hd.HD_BF16) // 2, N
+
+
+def test_noalloc_argument_errors(L):
+    """The allocation-free entry point validates like hd_infer_packed and
+    rejects a scratch need above its fixed size, all before any device call."""
+    sb = L.hd_noalloc_scratch_bytes()
+    assert sb == 4 << 20
+    f = L.hd_infer_packed_noalloc
+    assert f(FAKE, None, FAKE, None, 100, 8, 16, 3, 0, 0, None) == hd.HD_ERR_ARG
+    assert f(None, FAKE, FAKE, None, 100, 8, 16, 3, 0, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, None, 4, 0, 16, 3, 0, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, None, 4, 8, 16, 3, 9, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, None, 0, 8, 16, 3, 0, 0, None) == hd.HD_OK
+    N, F, D, K = 2000, 3072, 10240, 128
+    assert L.hd_infer_packed_workspace_bytes(N, F, D, K, hd.HD_BF16) > sb
+    assert f(FAKE, FAKE, FAKE, None, N, F, D, K, hd.HD_BF16, 0, None) == hd.HD_ERR_WORKSPACE
