@@ -135,6 +135,43 @@ hd_status hd_infer_packed(const void *X, const void *packed, int32_t *labels, fl
                           void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Streaming inference over a queue of small batches (the producer-consumer
+ * pipeline of Sec. III-A for the real-time streams of Sec. I, with the
+ * small-batch split of D of Sec. III-C Alg. 3): ONE persistent launch runs
+ * Alg. 1 on nbatch batches of N samples each, keeping the model's share of B
+ * in registers for the whole stream, so B is read once per launch rather
+ * than once per batch; while batch b is multiplied, batch b+1's X is loaded
+ * and batch b-1's partial scores are reduced.
+ *   X       [nbatch][N][F] fp32, batch b at X + b*N*F (4-byte aligned; 16-byte
+ *           aligned with N*F % 4 == 0 is faster).
+ *   packed  a model packed by hd_pack_model (fp32).
+ *   ready   NULL (every batch is present when the launch starts) or a 32-bit
+ *           counter in device memory or in mapped pinned host memory: batch b
+ *           is read only once *ready > b, with acquire ordering (write batch
+ *           b's X, then publish b+1 with release ordering). Setting bit 31
+ *           ends the stream after the batches already published. A batch not
+ *           published within about half a second also ends the stream.
+ *   labels  [nbatch][N] int32; scores [nbatch][N][K] fp32 or NULL.
+ *   done    NULL or a device/host-mapped counter that is incremented once
+ *           per batch whose labels (and scores) have been written.
+ *   workspace  hd_infer_stream_workspace_bytes(nbatch, ...) bytes, zeroed
+ *           before first use and left zeroed (one region per batch).
+ * Supported: fp32, 1 <= N <= 32, K <= 16, F <= 576, D <= 48 * (compute
+ * units - 1); otherwise HD_ERR_UNSUPPORTED (the workspace size query returns
+ * 0). The launch holds every compute unit but one with one workgroup each,
+ * plus one workgroup that reduces each batch's partial scores.
+ * Scores are summed with fp32 atomics (low bits may vary between runs).
+ * Results for batch b are complete once the launch finishes (or, with a
+ * queue, once *done > b as seen after a system-scope acquire).
+ */
+size_t hd_infer_stream_workspace_bytes(int64_t nbatch, int64_t N, int64_t F, int64_t D,
+                                       int64_t K, hd_dtype dt);
+hd_status hd_infer_stream(const void *X, const void *packed, const uint32_t *ready,
+                          int32_t *labels, float *scores, uint32_t *done, int64_t nbatch,
+                          int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,
+                          void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * hd_infer_packed without a caller workspace, for callers that cannot
  * allocate device memory or pass one in: code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation. It allocates

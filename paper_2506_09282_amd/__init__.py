@@ -34,6 +34,8 @@ SYMBOLS = (
     "hd_infer_kernel",
     "hd_noalloc_scratch_bytes",
     "hd_infer_packed_noalloc",
+    "hd_infer_stream_workspace_bytes",
+    "hd_infer_stream",
 )
 
 _lib = None
@@ -85,6 +87,11 @@ def lib():
         L.hd_noalloc_scratch_bytes.restype = sz
         L.hd_infer_packed_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, i32, vp]
         L.hd_infer_packed_noalloc.restype = i32
+        L.hd_infer_stream_workspace_bytes.argtypes = [i64, i64, i64, i64, i64, i32]
+        L.hd_infer_stream_workspace_bytes.restype = sz
+        L.hd_infer_stream.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i32, i32,
+                                      vp, sz, vp]
+        L.hd_infer_stream.restype = i32
         _lib = L
         return L
 
@@ -300,4 +307,51 @@ def infer_packed_noalloc(X, model: PackedModel, act: str = "hardsign", return_sc
                                        scores.data_ptr() if scores is not None else None, N, F, D,
                                        K, dt, ACTS[act], _stream_ptr(X.device))
     _raise(st, "hd_infer_packed_noalloc")
+    return (labels, scores) if (return_scores or out is not None) else labels
+
+
+def stream_workspace_bytes(nbatch: int, N: int, F: int, D: int, K: int, dtype) -> int:
+    torch = _torch()
+    dt = HD_F32 if dtype == torch.float32 else HD_BF16
+    return int(lib().hd_infer_stream_workspace_bytes(nbatch, N, F, D, K, dt))
+
+
+def infer_stream(X, model: PackedModel, act: str = "hardsign", return_scores: bool = False,
+                 ready=None, done=None, out=None, workspace=None):
+    """Streaming inference: ``X`` is [nbatch, N, F] (a queue of batches); one
+    persistent launch returns labels [nbatch, N] (and scores [nbatch, N, K]).
+
+    ``ready``/``done``: optional int32 tensors of one element (device memory
+    or pinned host memory) for the queue counter and the batches-done counter.
+    ``workspace``: a zeroed uint8 device tensor of at least
+    ``stream_workspace_bytes(...)`` bytes; otherwise a cached one is used."""
+    torch = _torch()
+    _check_dev(X)
+    if _dt(X) != model.dt:
+        raise TypeError("X dtype differs from the packed model's")
+    if X.dim() != 3:
+        raise ValueError("X must be [nbatch, N, F]")
+    nbatch, N, F = X.shape
+    if F != model.F:
+        raise ValueError("shape mismatch")
+    D, K, dt = model.D, model.K, model.dt
+    L = lib()
+    if out is not None:
+        labels, scores = out
+    else:
+        labels = torch.empty((nbatch, N), dtype=torch.int32, device=X.device)
+        scores = (torch.empty((nbatch, N, K), dtype=torch.float32, device=X.device)
+                  if return_scores else None)
+    need = int(L.hd_infer_stream_workspace_bytes(nbatch, N, F, D, K, dt))
+    if need == 0 and nbatch > 0:
+        raise HDError(HD_ERR_UNSUPPORTED, "hd_infer_stream")
+    ws = workspace if workspace is not None else _workspace(X.device, need,
+                                                            ("stream", nbatch, N, F, D, K, dt))
+    st = L.hd_infer_stream(X.data_ptr(), model.image.data_ptr(),
+                           ready.data_ptr() if ready is not None else None, labels.data_ptr(),
+                           scores.data_ptr() if scores is not None else None,
+                           done.data_ptr() if done is not None else None, nbatch, N, F, D, K, dt,
+                           ACTS[act], ws.data_ptr() if ws is not None else None,
+                           ws.numel() if ws is not None else 0, _stream_ptr(X.device))
+    _raise(st, "hd_infer_stream")
     return (labels, scores) if (return_scores or out is not None) else labels

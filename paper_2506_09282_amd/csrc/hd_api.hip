@@ -249,6 +249,34 @@ hd_status hd_infer_packed(const void* X, const void* packed, int32_t* labels, fl
                       workspace_bytes, stream);
 }
 
+size_t hd_infer_stream_workspace_bytes(int64_t nbatch, int64_t N, int64_t F, int64_t D,
+                                       int64_t K, hd_dtype dt) {
+  if (nbatch < 1 || N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) ||
+      !dims_ok(N, F, D, K) || nbatch > kMaxDim)
+    return 0;
+  if (!hd::stream_supported(N, F, D, K, dt)) return 0;
+  return hd::stream_ws_bytes(nbatch, N, K);
+}
+
+hd_status hd_infer_stream(const void* X, const void* packed, const uint32_t* ready,
+                          int32_t* labels, float* scores, uint32_t* done, int64_t nbatch,
+                          int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (nbatch < 0 || N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
+  if (!dims_ok(N, F, D, K) || nbatch > kMaxDim || nbatch * N > kMaxDim)
+    return HD_ERR_UNSUPPORTED;
+  if (nbatch == 0) return HD_OK;
+  if (!X || !packed || !labels || !workspace) return HD_ERR_ARG;
+  if (!aligned(X, 4) || !aligned(packed, 256) || !aligned(labels, 4) || !aligned(scores, 4) ||
+      !aligned(ready, 4) || !aligned(done, 4) || !aligned(workspace, 256))
+    return HD_ERR_ARG;
+  if (!hd::stream_supported(N, F, D, K, dt)) return HD_ERR_UNSUPPORTED;
+  if (workspace_bytes < hd::stream_ws_bytes(nbatch, N, K)) return HD_ERR_WORKSPACE;
+  const char* small = static_cast<const char*>(packed) + image_layout(F, D, K, dt).large;
+  return from_hip(hd::launch_stream(X, small, ready, labels, scores, done, nbatch, N, F, D, K,
+                                    act, workspace, stream));
+}
+
 // ---------------------------------------------------------------------------
 // hd_infer_packed_noalloc: hd_infer_packed with the library's own scratch.
 // The scratch is a file-scope device array: each GPU the library runs on

@@ -61,6 +61,16 @@ hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled,
 // may capture it in a graph).
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
 
+// Streaming inference: nbatch batches of N samples against a packed fp32
+// model whose share of B stays in registers (packed_small points at the
+// packed image's small-batch section).
+bool stream_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
+size_t stream_ws_bytes(int64_t nbatch, int64_t N, int64_t K);
+hipError_t launch_stream(const void* X, const void* packed_small, const unsigned* ready,
+                         int32_t* labels, float* scores, unsigned* done, int64_t nbatch,
+                         int64_t N, int64_t F, int64_t D, int64_t K, int act, void* workspace,
+                         hipStream_t stream);
+
 // Unfused stages.
 hipError_t launch_encode(const void* X, const void* B, float* H, int64_t N, int64_t F, int64_t D,
                          int dt, int act, hipStream_t stream);

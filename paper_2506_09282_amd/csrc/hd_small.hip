@@ -198,6 +198,40 @@ hipError_t pack_small_t(const void* B, const void* C, int64_t F, int64_t D, int6
 
 }  // namespace
 
+// Streaming plan: fp32, N <= 32, K <= 16, rows per lane at most 36 (F <= 576)
+// and at most three blocks per workgroup, so that a compute wave's share of
+// B (three blocks) and its X operands fit its registers. p.grid counts the
+// compute workgroups; the launch adds the reducer workgroup.
+static SmallPlan plan_stream(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  SmallPlan p{};
+  const int ms = frag_ms(F);
+  if (dt != 0 || N < 1 || N > 32 || K > kFragMaxK || ms < 1 || ms > 36) return p;
+  p.nblocks = (int)cdiv(D, kW);
+  // one compute unit is left to the reducer workgroup
+  const int cus = num_cus() > 1 ? num_cus() - 1 : 1;
+  p.grid = p.nblocks < cus ? p.nblocks : cus;
+  int64_t cslots = 1;
+  for (int b = 0; b < p.grid; ++b) {
+    const int c = block_walk(b, p.grid, p.nblocks).count();
+    cslots = c > cslots ? c : cslots;
+  }
+  if (cslots > 3) return p;
+  if ((int64_t)p.nblocks * K * kW * 4 >= ((int64_t)1 << 31)) return p;
+  const int nti = N <= 16 ? 1 : 2;
+  const int64_t nbk = 16 * nti;
+  const int64_t floats = (nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 +
+                         frag_cs_floats((int)cslots, (int)K) +
+                         frag_xs_floats((int)nbk, (int)F, ms);
+  // the reducer workgroup's eight per-wave sums use the same allocation
+  if (floats < 8 * nbk * K || (int64_t)sizeof(float) * floats > kLdsBudget) return p;
+  p.frag = true;
+  p.cslots = (int)cslots;
+  p.nb = nti;
+  p.ms = ms;
+  p.lds = sizeof(float) * (size_t)floats;
+  return p;
+}
+
 bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   return plan_valu(N, F, D, K, 8).nb > 0;
 }
@@ -239,6 +273,28 @@ hipError_t launch_pack_small(const void* B, const void* C, int64_t F, int64_t D,
   if (e != hipSuccess || frag_bytes(F, D, dt) == 0) return e;
   return launch_pack_frag(B, static_cast<char*>(out) + small_tiles_bytes(F, D, K, dt), F, D,
                           cdiv(D, kW), frag_ms(F), stream);
+}
+
+bool stream_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  return plan_stream(N, F, D, K, dt).frag;
+}
+
+size_t stream_ws_bytes(int64_t nbatch, int64_t N, int64_t K) {
+  return stream_workspace_bytes(nbatch, N, K);
+}
+
+hipError_t launch_stream(const void* X, const void* packed_small, const unsigned* ready,
+                         int32_t* labels, float* scores, unsigned* done, int64_t nbatch,
+                         int64_t N, int64_t F, int64_t D, int64_t K, int act, void* workspace,
+                         hipStream_t stream) {
+  const SmallPlan p = plan_stream(N, F, D, K, 0);
+  if (!p.frag || frag_bytes(F, D, 0) == 0) return hipErrorInvalidValue;
+  const char* base = static_cast<const char*>(packed_small);
+  const void* C = base + (cdiv(D, kW) * F * kW * 4 + 255) / 256 * 256;
+  const void* frag = base + small_tiles_bytes(F, D, K, 0);
+  const StreamArgs a{X, frag, C, ready, labels, scores, done, (int)nbatch, (int)N, (int)F,
+                     (int)K, act, workspace, stream};
+  return launch_stream_family(p, a);
 }
 
 hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled, int32_t* labels,

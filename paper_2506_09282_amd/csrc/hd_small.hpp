@@ -398,6 +398,34 @@ __device__ __forceinline__ int xcd_block(int b, int G) {
 constexpr int kFragThreads = 512;
 constexpr int kFragMaxK = 16;
 
+// LDS floats of the streaming kernel's C and X regions (the same column
+// split as the fragment kernel). C is filled in 1 KiB (256-float) pieces by
+// buffer-to-LDS loads, so both are rounded up to whole pieces; the X region
+// also holds a zeroed run of 16*MS floats after the X rows and 4 spare
+// floats.
+__host__ __device__ inline int frag_cs_floats(int cslots, int K) {
+  return (cslots * K * kW + 255) / 256 * 256;
+}
+__host__ __device__ inline int frag_xs_floats(int NB, int F, int MS) {
+  const int chunks = (NB * F / 4 + 63) / 64 * 256;
+  const int run = NB * F + 16 * MS;
+  return (chunks > run ? chunks : run) + 4;
+}
+
+// Streaming kernel (hd_stream.hip).
+struct StreamArgs {
+  const void *X, *frag, *C;
+  const unsigned* ready;
+  int32_t* labels;
+  float* scores;
+  unsigned* done;
+  int nbatch, N, F, K, act;
+  void* ws;
+  hipStream_t stream;
+};
+size_t stream_workspace_bytes(int64_t nbatch, int64_t N, int64_t K);
+hipError_t launch_stream_family(const SmallPlan& p, const StreamArgs& a);
+
 // Launchers, one translation unit per kernel family. Each applies the
 // plan (tile counts, steps, LDS bytes) to its kernel template.
 hipError_t launch_valu_family(SmallPlan& p, const Args& a, int dt, int lay);

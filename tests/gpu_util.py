@@ -60,6 +60,7 @@ def check_all_rows(X, B, C, y_gpu, S_gpu, chunk=4096, rtol=RTOL):
     S_gpu = None if S_gpu is None else np.asarray(S_gpu, dtype=np.float64)
     y_gpu = np.asarray(y_gpu)
     for r0 in range(0, N, chunk):
+        print(f"[rows] {r0}..{min(N, r0 + chunk)} of {N}", flush=True)
         rows = np.arange(r0, min(N, r0 + chunk))
         ref = oracle.infer(X, B, C, rows=rows)
         Sg = None if S_gpu is None else S_gpu[rows]
