@@ -49,6 +49,9 @@ class Oracle:
         lib.oracle_infer.argtypes = [_dp, _dp, _dp, _i64, _i64, _i64, _i64, ctypes.c_int, _lp,
                                      _i64, _ip, _dp, _dp, _dp, ctypes.c_int]
         lib.oracle_infer.restype = ctypes.c_int
+        lib.oracle_bundle.argtypes = [_dp, _dp, _ip, _i64, _i64, _i64, _i64, _lp, _dp,
+                                      ctypes.c_int]
+        lib.oracle_bundle.restype = ctypes.c_int
         lib.oracle_threads.argtypes = [ctypes.c_int]
         lib.oracle_threads.restype = ctypes.c_int
         self.lib = lib
@@ -113,6 +116,26 @@ class Oracle:
             out["A"] = A
         return out
 
+    def bundle(self, X, B, y, K: int, nthreads: int = 0):
+        """Single-pass training (Sec. II-C): dict with ``counts`` (int64 [K, D],
+        the per-class sums of the encoded bipolar hypervectors) and ``M``
+        (float64 [K, D], HardSign of the counts)."""
+        X, B = _f64(X), _f64(B)
+        N, F = X.shape
+        F2, D = B.shape
+        if F2 != F:
+            raise ValueError("shape mismatch")
+        yy = np.ascontiguousarray(np.asarray(y), dtype=np.int32)
+        if yy.shape != (N,):
+            raise ValueError("labels must be [N]")
+        counts = np.zeros((K, D), dtype=np.int64)
+        M = np.zeros((K, D), dtype=np.float64)
+        rc = self.lib.oracle_bundle(_ptr(X), _ptr(B), _ptr(yy, _ip), N, F, D, int(K),
+                                    _ptr(counts, _lp), _ptr(M), int(nthreads))
+        if rc != 0:
+            raise RuntimeError("oracle_bundle failed")
+        return {"counts": counts, "M": M}
+
     def similarity(self, H, C, nthreads: int = 0):
         """Stage II alone (Eq. 8 then Eq. 9) on a real matrix H: dict with y, S."""
         H, C = _f64(H), _f64(C)
@@ -157,3 +180,7 @@ def encode(X, B, act: str = "hardsign", want_va: bool = False, nthreads: int = 0
 
 def similarity(H, C, nthreads: int = 0):
     return default().similarity(H, C, nthreads=nthreads)
+
+
+def bundle(X, B, y, K: int, nthreads: int = 0):
+    return default().bundle(X, B, y, K, nthreads=nthreads)

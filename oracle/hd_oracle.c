@@ -183,5 +183,51 @@ int oracle_infer(const double *X, const double *B, const double *C, int64_t N, i
   return err ? -1 : 0;
 }
 
+/* Single-pass training (Sec. II-C): the class codebook row of class k is the
+ * normalised bundle (Sec. II-A bundling, then HardSign) of the encoded
+ * hypervectors (Eq. 2-3) of the samples labelled k:
+ *   counts[k,d] = sum over n with y[n] == k of HardSign(v[n,d])
+ *   M[k,d]      = HardSign(counts[k,d])
+ * A class with no sample, or a tied count, gives +1 (Eq. 1: ties to +1).
+ * Samples whose label lies outside [0, K) are skipped. counts are int64
+ * (exact); M may be NULL. Samples are encoded in parallel, chunk by chunk,
+ * and added in sample order. */
+int oracle_bundle(const double *X, const double *B, const int32_t *y, int64_t N, int64_t F,
+                  int64_t D, int64_t K, int64_t *counts, double *M, int nthreads) {
+  if (!X || !B || !y || !counts || N < 0 || F < 1 || D < 1 || K < 1) return -1;
+  for (int64_t i = 0; i < K * D; ++i) counts[i] = 0;
+  const int64_t chunk = 64;
+  double *h = (double *)malloc(sizeof(double) * (size_t)(chunk * D));
+  if (!h) return -1;
+  int err = 0;
+  const int nt = pick_threads(nthreads);
+  for (int64_t n0 = 0; n0 < N && !err; n0 += chunk) {
+    const int64_t n1 = n0 + chunk < N ? n0 + chunk : N;
+#pragma omp parallel num_threads(nt) reduction(| : err)
+    {
+      double *v = (double *)malloc(sizeof(double) * (size_t)D);
+      if (!v) {
+        err |= 1;
+      } else {
+#pragma omp for schedule(static)
+        for (int64_t n = n0; n < n1; ++n) {
+          encode_sample(X + n * F, B, F, D, v, NULL);
+          for (int64_t d = 0; d < D; ++d) h[(n - n0) * D + d] = hardsign(v[d]);
+        }
+      }
+      free(v);
+    }
+    for (int64_t n = n0; n < n1; ++n) {
+      const int32_t k = y[n];
+      if (k < 0 || k >= K) continue;
+      for (int64_t d = 0; d < D; ++d) counts[k * D + d] += (int64_t)h[(n - n0) * D + d];
+    }
+  }
+  free(h);
+  if (M)
+    for (int64_t i = 0; i < K * D; ++i) M[i] = hardsign((double)counts[i]);
+  return err ? -1 : 0;
+}
+
 /* Number of threads an OpenMP region started with `nthreads` would use. */
 int oracle_threads(int nthreads) { return pick_threads(nthreads); }
