@@ -193,6 +193,41 @@ hd_status hd_infer_packed_noalloc(const void *X, const void *packed, int32_t *la
                                   hd_dtype dt, hd_act act, hipStream_t stream);
 
 /*
+ * Single-pass training (Sec. II-C): the class hypervector of class k is the
+ * bundle (elementwise sum, Sec. II-A) of the encoded hypervectors
+ * H_n = HardSign(X_n B) (Eq. 2-3) of the samples with label k, normalised
+ * by HardSign (Eq. 1). The sums are exact integers, so training over many
+ * chunks of samples is two calls:
+ *
+ * hd_bundle_classes ADDS, for every sample n with 0 <= y[n] < K,
+ * HardSign(X_n B) (+1 or -1 per dimension, +1 for a zero product) into
+ * counts[y[n]][:]. Samples whose label lies outside [0, K) are skipped.
+ *   X       [N][F] row-major, dt; B [F][D] row-major, dt (element-aligned).
+ *   y       [N] int32 labels (device memory).
+ *   counts  [K][D] int32, device memory, caller-owned and caller-initialised
+ *           (zero it before the first chunk); calls on one stream
+ *           accumulate. |counts| never exceeds the number of samples seen,
+ *           so up to 2^31 - 1 samples per class are exact.
+ * The product is accumulated in fp32 (bf16 inputs are widened exactly), so
+ * a sample whose X_n B column lies within fp32 rounding of zero can take
+ * either sign, as in inference. Counters are added with integer atomics:
+ * the result is independent of their order.
+ * Supported: 1 <= K <= 512; N == 0 enqueues nothing.
+ *
+ * hd_class_hardsign writes M[k][d] = +1.0f if counts[k][d] >= 0, else
+ * -1.0f (Eq. 1; a tie or an empty class gives +1): the model C = M that
+ * hd_infer and hd_pack_model take, as [K][D] fp32.
+ * Both return HD_ERR_ARG for negative or zero sizes (N may be 0), NULL or
+ * misaligned pointers, HD_ERR_UNSUPPORTED outside the supported sizes,
+ * HD_ERR_HIP when a launch fails; nothing is enqueued on an error.
+ */
+hd_status hd_bundle_classes(const void *X, const void *B, const int32_t *y, int32_t *counts,
+                            int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt,
+                            hipStream_t stream);
+hd_status hd_class_hardsign(const int32_t *counts, float *M, int64_t K, int64_t D,
+                            hipStream_t stream);
+
+/*
  * Introspection: the name of the main kernel that hd_infer (packed == 0) or
  * hd_infer_packed (packed != 0) launches for these sizes, assuming 16-byte
  * aligned operands; "" when the call would be rejected. The returned string

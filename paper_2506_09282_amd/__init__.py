@@ -6,7 +6,8 @@ used for device memory and streams. There is no fallback: if the compiled
 library is missing, importing a function raises.
 
 Operation (ScalableHD, Alg. 1): H = HardSign(X B) (Eq. 7, Eq. 1),
-S = H C^T (Eq. 8), labels = argmax_k S (Eq. 9).
+S = H C^T (Eq. 8), labels = argmax_k S (Eq. 9). Single-pass training
+(Sec. II-C): C = HardSign of the per-class sums of HardSign(X B).
 """
 from __future__ import annotations
 
@@ -36,6 +37,8 @@ SYMBOLS = (
     "hd_infer_packed_noalloc",
     "hd_infer_stream_workspace_bytes",
     "hd_infer_stream",
+    "hd_bundle_classes",
+    "hd_class_hardsign",
 )
 
 _lib = None
@@ -92,6 +95,10 @@ def lib():
         L.hd_infer_stream.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i32, i32,
                                       vp, sz, vp]
         L.hd_infer_stream.restype = i32
+        L.hd_bundle_classes.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp]
+        L.hd_bundle_classes.restype = i32
+        L.hd_class_hardsign.argtypes = [vp, vp, i64, i64, vp]
+        L.hd_class_hardsign.restype = i32
         _lib = L
         return L
 
@@ -355,3 +362,56 @@ def infer_stream(X, model: PackedModel, act: str = "hardsign", return_scores: bo
                            ws.numel() if ws is not None else 0, _stream_ptr(X.device))
     _raise(st, "hd_infer_stream")
     return (labels, scores) if (return_scores or out is not None) else labels
+
+
+def bundle_classes(X, B, y, K: int, counts=None):
+    """Single-pass training, accumulation step (Sec. II-C): adds
+    HardSign(X_n B) into ``counts[y[n]]`` for every sample with 0 <= y[n] < K
+    and returns ``counts`` ([K, D] int32; a new zeroed tensor when None).
+    Calls with the same ``counts`` accumulate, so a training set can be fed
+    in chunks."""
+    torch = _torch()
+    _check_dev(X, B, y)
+    if X.dtype != B.dtype:
+        raise TypeError("X and B must have the same dtype")
+    if y.dtype != torch.int32:
+        raise TypeError("y must be int32")
+    N, F = X.shape
+    F2, D = B.shape
+    if F2 != F or y.shape != (N,):
+        raise ValueError("shape mismatch")
+    if counts is None:
+        counts = torch.zeros((K, D), dtype=torch.int32, device=X.device)
+    else:
+        _check_dev(counts)
+        if counts.dtype != torch.int32 or tuple(counts.shape) != (K, D):
+            raise ValueError("counts must be int32 [K, D]")
+    st = lib().hd_bundle_classes(X.data_ptr(), B.data_ptr(), y.data_ptr(), counts.data_ptr(), N,
+                                 F, D, K, _dt(X), _stream_ptr(X.device))
+    _raise(st, "hd_bundle_classes")
+    return counts
+
+
+def class_hardsign(counts, out=None):
+    """Normalisation step (Eq. 1): the class hypervectors M [K, D] float32,
+    +1 where counts >= 0 (ties and empty classes) and -1 elsewhere."""
+    torch = _torch()
+    _check_dev(counts)
+    if counts.dtype != torch.int32 or counts.dim() != 2:
+        raise ValueError("counts must be int32 [K, D]")
+    K, D = counts.shape
+    M = out if out is not None else torch.empty((K, D), dtype=torch.float32,
+                                                device=counts.device)
+    _check_dev(M)
+    if M.dtype != torch.float32 or tuple(M.shape) != (K, D):
+        raise ValueError("out must be float32 [K, D]")
+    st = lib().hd_class_hardsign(counts.data_ptr(), M.data_ptr(), K, D,
+                                 _stream_ptr(counts.device))
+    _raise(st, "hd_class_hardsign")
+    return M
+
+
+def train(X, B, y, K: int):
+    """Single-pass training in one call: M [K, D] float32 = class_hardsign(
+    bundle_classes(X, B, y, K))."""
+    return class_hardsign(bundle_classes(X, B, y, K))

@@ -277,6 +277,26 @@ hd_status hd_infer_stream(const void* X, const void* packed, const uint32_t* rea
                                     act, workspace, stream));
 }
 
+hd_status hd_bundle_classes(const void* X, const void* B, const int32_t* y, int32_t* counts,
+                            int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt,
+                            hipStream_t stream) {
+  if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0)) return HD_ERR_ARG;
+  if (!dims_ok(N, F, D, K) || !hd::bundle_supported(K)) return HD_ERR_UNSUPPORTED;
+  if (N == 0) return HD_OK;
+  if (!X || !B || !y || !counts) return HD_ERR_ARG;
+  if (!aligned(X, esize(dt)) || !aligned(B, esize(dt)) || !aligned(y, 4) || !aligned(counts, 4))
+    return HD_ERR_ARG;
+  return from_hip(hd::launch_bundle(X, B, y, counts, N, F, D, K, dt, stream));
+}
+
+hd_status hd_class_hardsign(const int32_t* counts, float* M, int64_t K, int64_t D,
+                            hipStream_t stream) {
+  if (K < 1 || D < 1) return HD_ERR_ARG;
+  if (!dims_ok(0, 1, D, K)) return HD_ERR_UNSUPPORTED;
+  if (!counts || !M || !aligned(counts, 4) || !aligned(M, 4)) return HD_ERR_ARG;
+  return from_hip(hd::launch_class_hardsign(counts, M, K, D, stream));
+}
+
 // ---------------------------------------------------------------------------
 // hd_infer_packed_noalloc: hd_infer_packed with the library's own scratch.
 // The scratch is a file-scope device array: each GPU the library runs on

@@ -71,6 +71,14 @@ hipError_t launch_stream(const void* X, const void* packed_small, const unsigned
                          int64_t N, int64_t F, int64_t D, int64_t K, int act, void* workspace,
                          hipStream_t stream);
 
+// Single-pass training (class sums of HardSign(X B), then their HardSign).
+constexpr int64_t kBundleMaxK = 512;
+bool bundle_supported(int64_t K);
+hipError_t launch_bundle(const void* X, const void* B, const int32_t* y, int32_t* counts,
+                         int64_t N, int64_t F, int64_t D, int64_t K, int dt, hipStream_t stream);
+hipError_t launch_class_hardsign(const int32_t* counts, float* M, int64_t K, int64_t D,
+                                 hipStream_t stream);
+
 // Unfused stages.
 hipError_t launch_encode(const void* X, const void* B, float* H, int64_t N, int64_t F, int64_t D,
                          int dt, int act, hipStream_t stream);

@@ -145,3 +145,28 @@ def test_noalloc_argument_errors(L):
     N, F, D, K = 2000, 3072, 10240, 128
     assert L.hd_infer_packed_workspace_bytes(N, F, D, K, hd.HD_BF16) > sb
     assert f(FAKE, FAKE, FAKE, None, N, F, D, K, hd.HD_BF16, 0, None) == hd.HD_ERR_WORKSPACE
+
+
+def test_training_argument_errors(L):
+    """hd_bundle_classes / hd_class_hardsign reject bad arguments before any
+    device call; N == 0 is a no-op."""
+    f = L.hd_bundle_classes
+    assert f(FAKE, FAKE, FAKE, FAKE, 0, 8, 64, 3, 0, None) == hd.HD_OK
+    assert f(None, None, None, None, 0, 8, 64, 3, 0, None) == hd.HD_OK
+    assert f(None, FAKE, FAKE, FAKE, 4, 8, 64, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, None, FAKE, 4, 8, 64, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, None, 4, 8, 64, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, FAKE, -1, 8, 64, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 0, 64, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 8, 0, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 8, 64, 0, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 8, 64, 3, 7, None) == hd.HD_ERR_ARG
+    assert f(FAKE + 2, FAKE, FAKE, FAKE, 4, 8, 64, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE + 2, FAKE, 4, 8, 64, 3, 1, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 8, 64, 513, 0, None) == hd.HD_ERR_UNSUPPORTED
+    g = L.hd_class_hardsign
+    assert g(None, FAKE, 3, 64, None) == hd.HD_ERR_ARG
+    assert g(FAKE, None, 3, 64, None) == hd.HD_ERR_ARG
+    assert g(FAKE, FAKE, 0, 64, None) == hd.HD_ERR_ARG
+    assert g(FAKE, FAKE, 3, 0, None) == hd.HD_ERR_ARG
+    assert g(FAKE + 1, FAKE, 3, 64, None) == hd.HD_ERR_ARG

@@ -1,0 +1,190 @@
+"""GPU parity of single-pass training (Sec. II-C): hd_bundle_classes and
+hd_class_hardsign (through the C ABI) against the oracle's bundle.
+
+On small-integer inputs the encoding sums are exact in any order, so the
+class counts and the codebook must be bit-identical. On real-valued inputs a
+sample whose encoding sum lies within fp32 rounding distance of zero (the
+fragile set of tolerance.py) may take either sign: the count of class k at
+dimension d may then differ from the oracle's by 2 per such sample of class
+k, and nowhere else; the codebook must be HardSign of the GPU's own counts,
+and equal to the oracle's wherever the oracle's count is farther from zero
+than those flips could move it.
+"""
+import numpy as np
+import pytest
+
+import hd_inputs
+import oracle
+from gpu_util import announce, dev, torch_or_skip
+from tolerance import gamma
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def hd():
+    torch_or_skip()
+    import paper_2506_09282_amd as hd
+    hd.lib()
+    return hd
+
+
+def labels_for(N, K, seed, spill=0):
+    """Labels in [0, K); ``spill`` of them replaced by values outside it."""
+    g = np.random.default_rng(seed + 17)
+    y = g.integers(0, K, N).astype(np.int32)
+    if spill:
+        idx = g.choice(N, size=min(spill, N), replace=False)
+        y[idx] = g.choice(np.array([-1, K, K + 5, -(1 << 30), (1 << 30)], np.int32), len(idx))
+    return y
+
+
+def gpu_train(hd, X, B, y, K, dtype, chunks=1):
+    torch = torch_or_skip()
+    Xd, Bd = dev(X, dtype), dev(B, dtype)
+    yd = torch.from_numpy(np.ascontiguousarray(y, np.int32)).cuda()
+    counts = None
+    N = X.shape[0]
+    cuts = np.linspace(0, N, chunks + 1).astype(int)
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        if counts is None:
+            counts = torch.zeros((K, B.shape[1]), dtype=torch.int32, device="cuda")
+        hd.bundle_classes(Xd[a:b], Bd, yd[a:b], K, counts=counts)
+    M = hd.class_hardsign(counts)
+    torch.cuda.synchronize()
+    return counts.cpu().numpy().astype(np.int64), M.cpu().numpy().astype(np.float64)
+
+
+def check_exact(counts, M, ref):
+    assert np.array_equal(counts, ref["counts"]), np.abs(counts - ref["counts"]).max()
+    assert np.array_equal(M, ref["M"])
+
+
+def check_fragile(counts, M, X, B, y, K, ref):
+    """The rule of the module docstring; returns the number of differing
+    counts (for the log)."""
+    enc = oracle.encode(X, B, want_va=True)
+    fragile = np.abs(enc["V"]) <= gamma(X.shape[1]) * enc["A"]
+    nf = np.zeros(counts.shape, np.int64)
+    for k in range(K):
+        sel = y == k
+        if sel.any():
+            nf[k] = fragile[sel].sum(axis=0)
+    diff = counts - ref["counts"]
+    assert np.all(diff % 2 == 0)
+    assert np.all(np.abs(diff) <= 2 * nf), int((np.abs(diff) - 2 * nf).max())
+    assert np.array_equal(M, np.where(counts >= 0, 1.0, -1.0))
+    sure = np.abs(ref["counts"]) > 2 * nf
+    assert np.array_equal(M[sure], ref["M"][sure])
+    return int((diff != 0).sum())
+
+
+# (N, F, D, K, spill): ragged sample tiles and column blocks, one class,
+# more classes than samples (empty classes), the largest supported K, and
+# labels outside [0, K).
+INTEGER = [
+    (1, 5, 64, 1, 0),
+    (63, 7, 100, 3, 0),
+    (64, 561, 10240, 6, 0),
+    (1000, 561, 10240, 6, 25),
+    (777, 617, 4999, 26, 10),
+    (130, 3072, 1024, 100, 3),
+    (50, 40, 300, 80, 0),
+    (2100, 33, 640, 512, 40),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,F,D,K,spill", INTEGER)
+def test_integer_counts_bit_exact(hd, N, F, D, K, spill, dtype):
+    announce(f"train integer {dtype} N={N} F={F} D={D} K={K} spill={spill}")
+    X, B, _ = hd_inputs.make_integer_inputs(N, F, D, 1, seed=N + F + K)
+    y = labels_for(N, K, N + K, spill)
+    ref = oracle.bundle(X, B, y, K)
+    counts, M = gpu_train(hd, X, B, y, K, dtype)
+    check_exact(counts, M, ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_zero_sums_and_tied_counts(hd, dtype):
+    """X and B in {-1, 0, 1}: many encoding sums are exactly 0 (HardSign gives
+    +1) and many class counts are exactly 0 (the codebook gives +1)."""
+    N, F, D, K = 700, 40, 1000, 9
+    announce(f"train ties {dtype} N={N} F={F} D={D} K={K}")
+    X, B, _ = hd_inputs.make_integer_inputs(N, F, D, 1, seed=5, x_range=1, b_range=1)
+    y = labels_for(N, K, 5)
+    y[y == 4] = 3  # class 4 is empty: all +1
+    ref = oracle.bundle(X, B, y, K)
+    assert (ref["counts"] == 0).sum() > 100
+    counts, M = gpu_train(hd, X, B, y, K, dtype)
+    check_exact(counts, M, ref)
+    assert np.all(M[4] == 1.0) and np.all(counts[4] == 0)
+
+
+# Real-valued inputs at the workload shapes (features, hypervector width,
+# classes), with a few thousand samples.
+REAL = [
+    ("activity", 2000, 561, 10240, 6, "uniform_pm1", "f32"),
+    ("image", 1500, 617, 10240, 26, "uniform01", "f32"),
+    ("image", 1500, 617, 10240, 26, "uniform01", "bf16"),
+    ("colour", 600, 3072, 4096, 10, "uniform01", "bf16"),
+    ("colour_k100", 600, 3072, 2048, 100, "uniform01_zero20", "f32"),
+]
+
+
+@pytest.mark.parametrize("name,N,F,D,K,dist,dtype", REAL)
+def test_real_inputs_within_fragile_flips(hd, name, N, F, D, K, dist, dtype):
+    announce(f"train real {name} {dtype} N={N} F={F} D={D} K={K}")
+    X, B, _ = hd_inputs.make_inputs(N, F, D, 1, dist, seed=3, dtype=dtype)
+    y = labels_for(N, K, 3)
+    ref = oracle.bundle(X, B, y, K)
+    counts, M = gpu_train(hd, X, B, y, K, dtype)
+    ndiff = check_fragile(counts, M, X, B, y, K, ref)
+    print(f"[train] {name}: {ndiff} of {counts.size} counts differ (fragile samples)")
+
+
+@pytest.mark.parametrize("chunks", [2, 7])
+def test_chunked_accumulation_equals_one_call(hd, chunks):
+    """Counts are integers added with atomics: feeding the samples in chunks
+    gives the same counts bit for bit, on real-valued inputs too."""
+    N, F, D, K = 1300, 561, 2048, 6
+    announce(f"train chunks={chunks} N={N}")
+    X, B, _ = hd_inputs.make_inputs(N, F, D, 1, "uniform_pm1", seed=9)
+    y = labels_for(N, K, 9)
+    c1, m1 = gpu_train(hd, X, B, y, K, "f32", chunks=1)
+    ck, mk = gpu_train(hd, X, B, y, K, "f32", chunks=chunks)
+    assert np.array_equal(c1, ck)
+    assert np.array_equal(m1, mk)
+
+
+def test_empty_batch_leaves_counts(hd):
+    torch = torch_or_skip()
+    counts = torch.full((3, 64), 7, dtype=torch.int32, device="cuda")
+    X = torch.empty((0, 5), dtype=torch.float32, device="cuda")
+    B = torch.ones((5, 64), dtype=torch.float32, device="cuda")
+    y = torch.empty((0,), dtype=torch.int32, device="cuda")
+    hd.bundle_classes(X, B, y, 3, counts=counts)
+    torch.cuda.synchronize()
+    assert bool((counts == 7).all())
+
+
+def test_single_sample_classes_round_trip(hd):
+    """One sample per class: each codebook row is that sample's encoding, so
+    inference on the same samples scores exactly D on the own class and
+    returns the sample's label (planted classes; the closed form pinned on
+    the oracle)."""
+    torch = torch_or_skip()
+    K, F, D = 12, 561, 10240
+    announce(f"train round trip K={K} F={F} D={D}")
+    X, B, _ = hd_inputs.make_integer_inputs(K, F, D, 1, seed=4)
+    y = np.arange(K, dtype=np.int32)[::-1].copy()
+    counts, M = gpu_train(hd, X, B, y, K, "f32")
+    H = oracle.encode(X, B)["H"]
+    assert np.array_equal(M[y], H)
+    Xd = dev(X, "f32")
+    Md = torch.from_numpy(M.astype(np.float32)).cuda()
+    labels, S = hd.infer(Xd, dev(B, "f32"), Md, return_scores=True)
+    torch.cuda.synchronize()
+    S = S.cpu().numpy()
+    assert np.array_equal(labels.cpu().numpy(), y)
+    assert np.all(S[np.arange(K), y] == D)
