@@ -116,7 +116,9 @@ hd_status hd_infer(const void *X, const void *B, const void *C, int32_t *labels,
  * One-time model tiling (Sec. III-D: B and J = M^T stored in the block order
  * the consumer reads them). The packed image is opaque; its size depends only
  * on (F, D, K, dt). packed must be a device buffer of at least
- * hd_model_packed_bytes(F, D, K, dt) bytes.
+ * hd_model_packed_bytes(F, D, K, dt) bytes. C may be NULL before the class
+ * hypervectors exist (a model packed for hd_bundle_classes_packed): the class
+ * part of the image is then zero.
  */
 size_t hd_model_packed_bytes(int64_t F, int64_t D, int64_t K, hd_dtype dt);
 hd_status hd_pack_model(const void *B, const void *C, int64_t F, int64_t D, int64_t K, hd_dtype dt,
@@ -226,6 +228,19 @@ hd_status hd_bundle_classes(const void *X, const void *B, const int32_t *y, int3
                             hipStream_t stream);
 hd_status hd_class_hardsign(const int32_t *counts, float *M, int64_t K, int64_t D,
                             hipStream_t stream);
+
+/*
+ * hd_bundle_classes on the matrix cores, reading B from a model packed by
+ * hd_pack_model with the same (F, D, dt) (the tiled B of Sec. III-D; the
+ * image's class part is not read, so it may have been packed with C == NULL
+ * and any K). Same arguments, semantics and errors as hd_bundle_classes, and
+ * bit-identical counts wherever no product lies within rounding of zero
+ * (both accumulate in fp32, in different orders).
+ * Supported: 1 <= K <= 128, N <= 2^30.
+ */
+hd_status hd_bundle_classes_packed(const void *X, const void *packed, const int32_t *y,
+                                   int32_t *counts, int64_t N, int64_t F, int64_t D, int64_t K,
+                                   hd_dtype dt, hipStream_t stream);
 
 /*
  * Introspection: the name of the main kernel that hd_infer (packed == 0) or

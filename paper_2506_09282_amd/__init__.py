@@ -39,6 +39,7 @@ SYMBOLS = (
     "hd_infer_stream",
     "hd_bundle_classes",
     "hd_class_hardsign",
+    "hd_bundle_classes_packed",
 )
 
 _lib = None
@@ -99,6 +100,8 @@ def lib():
         L.hd_bundle_classes.restype = i32
         L.hd_class_hardsign.argtypes = [vp, vp, i64, i64, vp]
         L.hd_class_hardsign.restype = i32
+        L.hd_bundle_classes_packed.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp]
+        L.hd_bundle_classes_packed.restype = i32
         _lib = L
         return L
 
@@ -244,21 +247,26 @@ class PackedModel:
         self.image, self.F, self.D, self.K, self.dt = image, F, D, K, dt
 
 
-def pack_model(B, C) -> PackedModel:
+def pack_model(B, C=None, K: int = 1) -> PackedModel:
+    """Tile B and C once (Sec. III-D). ``C=None`` packs B alone (the class
+    part of the image is zero, sized for ``K`` classes): a model for
+    ``bundle_classes_packed`` before the class hypervectors exist."""
     torch = _torch()
-    _check_dev(B, C)
-    if B.dtype != C.dtype:
-        raise TypeError("B and C must share a dtype")
+    _check_dev(B)
     F, D = B.shape
-    K, D2 = C.shape
-    if D2 != D:
-        raise ValueError("shape mismatch")
+    if C is not None:
+        _check_dev(C)
+        if B.dtype != C.dtype:
+            raise TypeError("B and C must share a dtype")
+        K, D2 = C.shape
+        if D2 != D:
+            raise ValueError("shape mismatch")
     dt = _dt(B)
     L = lib()
     nbytes = int(L.hd_model_packed_bytes(F, D, K, dt))
     image = torch.empty(nbytes, dtype=torch.uint8, device=B.device)
-    st = L.hd_pack_model(B.data_ptr(), C.data_ptr(), F, D, K, dt, image.data_ptr(), nbytes,
-                         _stream_ptr(B.device))
+    st = L.hd_pack_model(B.data_ptr(), C.data_ptr() if C is not None else None, F, D, K, dt,
+                         image.data_ptr(), nbytes, _stream_ptr(B.device))
     _raise(st, "hd_pack_model")
     return PackedModel(image, F, D, K, dt)
 
@@ -389,6 +397,32 @@ def bundle_classes(X, B, y, K: int, counts=None):
     st = lib().hd_bundle_classes(X.data_ptr(), B.data_ptr(), y.data_ptr(), counts.data_ptr(), N,
                                  F, D, K, _dt(X), _stream_ptr(X.device))
     _raise(st, "hd_bundle_classes")
+    return counts
+
+
+def bundle_classes_packed(X, model: PackedModel, y, K: int, counts=None):
+    """``bundle_classes`` on the matrix cores, reading B from a packed model
+    (``pack_model(B)`` or ``pack_model(B, C)``; the class part is not read)."""
+    torch = _torch()
+    _check_dev(X, y)
+    if _dt(X) != model.dt:
+        raise TypeError("X dtype differs from the packed model's")
+    if y.dtype != torch.int32:
+        raise TypeError("y must be int32")
+    N, F = X.shape
+    if F != model.F or y.shape != (N,):
+        raise ValueError("shape mismatch")
+    D = model.D
+    if counts is None:
+        counts = torch.zeros((K, D), dtype=torch.int32, device=X.device)
+    else:
+        _check_dev(counts)
+        if counts.dtype != torch.int32 or tuple(counts.shape) != (K, D):
+            raise ValueError("counts must be int32 [K, D]")
+    st = lib().hd_bundle_classes_packed(X.data_ptr(), model.image.data_ptr(), y.data_ptr(),
+                                        counts.data_ptr(), N, F, D, K, model.dt,
+                                        _stream_ptr(X.device))
+    _raise(st, "hd_bundle_classes_packed")
     return counts
 
 

@@ -155,7 +155,7 @@ hd_status hd_pack_model(const void* B, const void* C, int64_t F, int64_t D, int6
                         void* packed, size_t packed_bytes, hipStream_t stream) {
   if (F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0)) return HD_ERR_ARG;
   if (!dims_ok(0, F, D, K)) return HD_ERR_UNSUPPORTED;
-  if (!B || !C || !packed) return HD_ERR_ARG;
+  if (!B || !packed) return HD_ERR_ARG;  // C may be NULL: a model packed for training
   if (!aligned(B, esize(dt)) || !aligned(C, esize(dt)) || !aligned(packed, 256)) return HD_ERR_ARG;
   const Image im = image_layout(F, D, K, dt);
   if (packed_bytes < im.total) return HD_ERR_WORKSPACE;
@@ -287,6 +287,19 @@ hd_status hd_bundle_classes(const void* X, const void* B, const int32_t* y, int3
   if (!aligned(X, esize(dt)) || !aligned(B, esize(dt)) || !aligned(y, 4) || !aligned(counts, 4))
     return HD_ERR_ARG;
   return from_hip(hd::launch_bundle(X, B, y, counts, N, F, D, K, dt, stream));
+}
+
+hd_status hd_bundle_classes_packed(const void* X, const void* packed, const int32_t* y,
+                                   int32_t* counts, int64_t N, int64_t F, int64_t D, int64_t K,
+                                   hd_dtype dt, hipStream_t stream) {
+  if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0)) return HD_ERR_ARG;
+  if (!dims_ok(N, F, D, K)) return HD_ERR_UNSUPPORTED;
+  if (N > 0 && !hd::bundle_packed_supported(N, F, D, K, dt)) return HD_ERR_UNSUPPORTED;
+  if (N == 0) return HD_OK;
+  if (!X || !packed || !y || !counts) return HD_ERR_ARG;
+  if (!aligned(X, esize(dt)) || !aligned(packed, 256) || !aligned(y, 4) || !aligned(counts, 4))
+    return HD_ERR_ARG;
+  return from_hip(hd::launch_bundle_packed(X, packed, y, counts, N, F, D, K, dt, stream));
 }
 
 hd_status hd_class_hardsign(const int32_t* counts, float* M, int64_t K, int64_t D,

@@ -78,6 +78,13 @@ hipError_t launch_bundle(const void* X, const void* B, const int32_t* y, int32_t
                          int64_t N, int64_t F, int64_t D, int64_t K, int dt, hipStream_t stream);
 hipError_t launch_class_hardsign(const int32_t* counts, float* M, int64_t K, int64_t D,
                                  hipStream_t stream);
+// The same class sums on the matrix cores, from the tiled B of a packed model
+// (the large-batch section at the start of the image).
+constexpr int64_t kBundleMfmaMaxK = 128;
+bool bundle_packed_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
+hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t* y,
+                                int32_t* counts, int64_t N, int64_t F, int64_t D, int64_t K,
+                                int dt, hipStream_t stream);
 
 // Unfused stages.
 hipError_t launch_encode(const void* X, const void* B, float* H, int64_t N, int64_t F, int64_t D,

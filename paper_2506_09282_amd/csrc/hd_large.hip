@@ -1117,6 +1117,235 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Single-pass training on the matrix cores (Sec. II-C): the class sums
+// counts[k][d] += sum over samples n of class k of HardSign(X_n B)[d], from
+// the tiled B of a packed model.
+//
+// Stage I is computed here as V = X B, not transposed: the same fragments as
+// inference with the two operands exchanged, so the sample n is the MFMA row
+// index and the hypervector dimension d the column index. Each lane then ends
+// with 16 samples of one column, and the 32 lanes of a half-wave hold 32
+// consecutive columns of one sample: the class-counter adds in LDS touch 32
+// consecutive words of one class row per instruction, free of bank and
+// address conflicts.
+//
+// A work item is (sample tile of NT samples, column group of 256 = one
+// 64-column unit per wave). A workgroup takes one column group and a
+// contiguous range of sample tiles; each tile's X streams through LDS in
+// chunks of fsc f-steps while V stays in registers across the chunks, and the
+// workgroup's class counters [K][256] stay in LDS until its last tile, then
+// are added into the caller's counts with one device atomic per nonzero
+// counter.
+// ---------------------------------------------------------------------------
+constexpr int kBundleCols = 64 * kWaves;
+constexpr int kBundleStageBatch = 4;  // staging items per thread per batch
+
+// Stage f-steps [fs0, fs0 + fsn) of rows n0 .. n0 + rows - 1 of X into the
+// LDS tile (row pitch `pitch` elements), zero past F; rows past `rows` are
+// not written (their labels are invalid, so their V is never used).
+template <class Tr, int NT>
+__device__ __forceinline__ void bundle_stage(typename Tr::elem* xt, const typename Tr::elem* X,
+                                             int F, int64_t n0, int rows, int fs0, int fsn,
+                                             int pitch, bool vec, int tid) {
+  typedef typename Tr::elem T;
+  constexpr int kSB = kBundleStageBatch;
+  const int items = NT * fsn;
+  for (int base = 0; base < items; base += kThreads * kSB) {
+    uint4 w[kSB][2];
+#pragma unroll
+    for (int j = 0; j < kSB; ++j) {
+      const int i = base + j * kThreads + tid;
+      const int r = i / fsn, s = i - r * fsn;
+      const int rr = r < rows ? r : rows - 1;  // clamped into X, masked below
+      const T* xr = X + (n0 + rr) * (int64_t)F;
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const int c = (fs0 + s) * Tr::kFStep + g * Tr::kVec;
+        if (vec) {
+          const int cc = c < F ? c : F - Tr::kVec;
+          w[j][g] = *reinterpret_cast<const uint4*>(xr + cc);
+        } else {
+          uint32_t t[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+          for (int e = 0; e < Tr::kVec; ++e) {
+            const int ce = c + e < F ? c + e : F - 1;
+            const T x = xr[ce];
+            if constexpr (Tr::kEsz == 2)
+              t[e >> 1] |= (uint32_t)x << (16 * (e & 1));
+            else
+              t[e] = __float_as_uint(x);
+          }
+          w[j][g] = make_uint4(t[0], t[1], t[2], t[3]);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kSB; ++j) {
+      const int i = base + j * kThreads + tid;
+      if (i >= items) break;
+      const int r = i / fsn, s = i - r * fsn;
+      if (r >= rows) continue;
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const int c = (fs0 + s) * Tr::kFStep + g * Tr::kVec;
+        if (c >= F) {
+          w[j][g] = make_uint4(0u, 0u, 0u, 0u);
+        } else if (c + Tr::kVec > F) {  // ragged last group (F % kVec != 0)
+          uint32_t t[4] = {w[j][g].x, w[j][g].y, w[j][g].z, w[j][g].w};
+#pragma unroll
+          for (int e = 0; e < Tr::kVec; ++e)
+            if (c + e >= F) {
+              if constexpr (Tr::kEsz == 2)
+                t[e >> 1] &= ~(0xffffu << (16 * (e & 1)));
+              else
+                t[e] = 0u;
+            }
+          w[j][g] = make_uint4(t[0], t[1], t[2], t[3]);
+        }
+      }
+      uint4* dst = reinterpret_cast<uint4*>(xt + r * pitch + s * Tr::kFStep);
+      if constexpr (Tr::kEsz == 2) {
+        dst[0] = w[j][0];
+        dst[1] = w[j][1];
+      } else {
+        dst[0] = make_uint4(w[j][0].x, w[j][0].z, w[j][1].x, w[j][1].z);
+        dst[1] = make_uint4(w[j][0].y, w[j][0].w, w[j][1].y, w[j][1].w);
+      }
+    }
+  }
+}
+
+template <class Tr, int NTILES, int OCC>
+__global__ __launch_bounds__(kThreads, OCC) void bundle_mfma_kernel(
+    const typename Tr::elem* __restrict__ X, const uint4* __restrict__ Bp,
+    const int32_t* __restrict__ y, int32_t* __restrict__ counts, int N, int F, int D, int K,
+    int ndb, int ngroups, int fsc) {
+  typedef typename Tr::elem T;
+  constexpr int NT = 32 * NTILES;
+  constexpr int kPrefetch = prefetch_of(NTILES, 1);
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nfs = nfs_of<Tr>(F);
+  const int nchunks = (nfs + fsc - 1) / fsc;
+  const int pitch = fsc * Tr::kFStep + (Tr::kEsz == 2 ? 8 : 4);  // elements
+  const int units = ndb / 2;
+  const int ncg = (units + kWaves - 1) / kWaves;
+  const int cg = blockIdx.x % ncg;
+  const int sg = blockIdx.x / ncg;
+  const int ntiles = (N + NT - 1) / NT;
+  const int t_begin = (int)((int64_t)ntiles * sg / ngroups);
+  const int t_end = (int)((int64_t)ntiles * (sg + 1) / ngroups);
+
+  // LDS: [X chunk tile NT x pitch | 16-byte zero slot | labels NT | counters K x 256]
+  T* xt = reinterpret_cast<T*>(lds);
+  const size_t xbytes = (size_t)NT * pitch * sizeof(T) + 16;
+  const T* xzero = xt + NT * pitch;
+  int* ys = reinterpret_cast<int*>(lds + xbytes);
+  int* cnt = ys + NT;
+  for (int i = tid; i < K * kBundleCols; i += kThreads) cnt[i] = 0;
+  if (tid == 0) *reinterpret_cast<uint4*>(xt + NT * pitch) = make_uint4(0u, 0u, 0u, 0u);
+
+  const int u = cg * kWaves + wave;
+  const bool valid = u < units;
+  const int uu = valid ? u : cg * kWaves;  // waves without a unit compute and discard
+  const int xrow = lane & 31, xhalf = lane >> 5;
+  const T* xlane = xt + xrow * pitch + xhalf * (Tr::kFStep / 2);
+  const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(Bp), 0, ndb * nfs * 1024, 0x00020000);
+  auto bfrag = [&](int fs, int b) -> uint4 {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         brsrc, ((2 * uu + b) * nfs + fs) * 1024 + lane * 16, 0, 0));
+  };
+  const bool vec = (F % Tr::kVec) == 0 && ((uintptr_t)X % 16) == 0;
+
+  for (int tile = t_begin; tile < t_end; ++tile) {
+    const int64_t n0 = (int64_t)tile * NT;
+    const int rows = (int)min((int64_t)NT, (int64_t)N - n0);
+    f32x16 vacc[2][NTILES];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) vacc[b][t][r] = 0.0f;
+
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const int fs0 = ch * fsc;
+      const int fsn = min(fsc, nfs - fs0);
+      __syncthreads();  // the previous chunk's (and tile's) readers are done
+      if (ch == 0 && tid < NT) {
+        int k = -1;
+        if (tid < rows) {
+          k = y[n0 + tid];
+          if (k < 0 || k >= K) k = -1;  // labels outside [0, K) are skipped
+        }
+        ys[tid] = k;
+      }
+      bundle_stage<Tr, NT>(xt, X, F, n0, rows, fs0, fsn, pitch, vec, tid);
+      __syncthreads();
+      uint4 afr[kPrefetch][2];
+#pragma unroll
+      for (int i = 0; i < kPrefetch; ++i) {
+        afr[i][0] = bfrag(fs0 + (i < fsn ? i : fsn - 1), 0);
+        afr[i][1] = bfrag(fs0 + (i < fsn ? i : fsn - 1), 1);
+      }
+      uint4 xfr[2][NTILES];
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t)
+        xfr[0][t] = *reinterpret_cast<const uint4*>(xlane + t * 32 * pitch);
+      const int fsl = (fsn + kPrefetch - 1) / kPrefetch * kPrefetch;
+      // Branch-free steps as in inference: padding steps past fsn multiply a
+      // valid B fragment by the zero slot.
+      for (int s0 = 0; s0 < fsl; s0 += kPrefetch) {
+#pragma unroll
+        for (int i = 0; i < kPrefetch; ++i) {
+          const int fs = s0 + i;
+          const int fsx = fs + 1;
+#pragma unroll
+          for (int t = 0; t < NTILES; ++t)
+            xfr[(i + 1) & 1][t] = *reinterpret_cast<const uint4*>(
+                fsx < fsn ? xlane + t * 32 * pitch + fsx * Tr::kFStep : xzero);
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int t = 0; t < NTILES; ++t) Tr::stage1(vacc[b][t], xfr[i & 1][t], afr[i][b]);
+          __builtin_amdgcn_sched_group_barrier(0x100, NTILES, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES * Tr::kStage1Mfma, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+          const int nx = fs + kPrefetch;
+          afr[i][0] = bfrag(fs0 + (nx < fsn ? nx : fsn - 1), 0);
+          afr[i][1] = bfrag(fs0 + (nx < fsn ? nx : fsn - 1), 1);
+        }
+      }
+    }
+    // HardSign (Eq. 1) and the class sums. Accumulator r of lane l is row
+    // 8(r/4) + 4(l/32) + r%4 (a sample) of column l%32 (a dimension).
+    if (valid) {
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int k = ys[32 * t + 8 * (r >> 2) + 4 * xhalf + (r & 3)];
+          if (k >= 0) {
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+              atomicAdd(&cnt[k * kBundleCols + wave * 64 + 32 * b + xrow],
+                        vacc[b][t][r] >= 0.0f ? 1 : -1);
+          }
+        }
+    }
+  }
+  __syncthreads();
+  const int64_t d0 = (int64_t)cg * kBundleCols;
+  for (int i = tid; i < K * kBundleCols; i += kThreads) {
+    const int k = i / kBundleCols, c = i % kBundleCols;
+    const int v = cnt[i];
+    if (v != 0 && d0 + c < D) atomicAdd(&counts[(int64_t)k * D + d0 + c], v);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host-side configuration.
 // ---------------------------------------------------------------------------
 struct LargeCfg {
@@ -1188,13 +1417,13 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) 
   return c;
 }
 
-// Lets kernel k use kLdsBytes of dynamic LDS on the current device (set once
+// Lets a kernel use kLdsBytes of dynamic LDS on the current device (set once
 // per device and kernel).
-template <typename KernelT>
-hipError_t allow_large_lds(KernelT* k) {
-  static PerDeviceOnce once;
-  return once_per_device(once, [k] {
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+template <auto Kernel>
+hipError_t allow_large_lds() {
+  static PerDeviceOnce once;  // one per kernel: the template argument is its address
+  return once_per_device(once, [] {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(Kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
   });
 }
@@ -1207,7 +1436,7 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
   if (c.fsc > 0) {
     if (c.dma) {
       if constexpr (Tr::kEsz == 2 && NTILES == kDmaNtiles) {
-        const hipError_t dattr = allow_large_lds(&large_chunked_dma_kernel<NTILES, KB, ACT>);
+        const hipError_t dattr = allow_large_lds<&large_chunked_dma_kernel<NTILES, KB, ACT>>();
         if (dattr != hipSuccess) return dattr;
         hipLaunchKernelGGL((large_chunked_dma_kernel<NTILES, KB, ACT>), grid, block, c.lds,
                            stream, (const bf16raw*)X, Bp, Cp, labels, scores, (int)N, (int)F,
@@ -1217,7 +1446,7 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
       return hipErrorInvalidValue;
     }
     if constexpr (NTILES == chunk_ntiles<Tr>(KB)) {
-      const hipError_t cattr = allow_large_lds(&large_chunked_kernel<Tr, NTILES, KB, ACT>);
+      const hipError_t cattr = allow_large_lds<&large_chunked_kernel<Tr, NTILES, KB, ACT>>();
       if (cattr != hipSuccess) return cattr;
       hipLaunchKernelGGL((large_chunked_kernel<Tr, NTILES, KB, ACT>), grid, block, c.lds, stream,
                          (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F,
@@ -1226,7 +1455,7 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
     }
     return hipErrorInvalidValue;
   }
-  const hipError_t attr = allow_large_lds(&large_fused_kernel<Tr, NTILES, KB, ACT>);
+  const hipError_t attr = allow_large_lds<&large_fused_kernel<Tr, NTILES, KB, ACT>>();
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((large_fused_kernel<Tr, NTILES, KB, ACT>), grid, block, c.lds, stream,
                      (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F, (int)K,
@@ -1268,7 +1497,79 @@ hipError_t launch_tr(const void* X, const void* packed, int32_t* labels, float* 
   return hipErrorInvalidValue;
 }
 
+// Training plan: NTILES sample tiles of 32 per workgroup, f-steps per X
+// chunk, workgroups per compute unit (from LDS and registers), and the
+// number of sample-tile groups.
+struct BundleCfg {
+  int nt, occ, fsc, ngroups, ncg;
+  size_t lds;
+  bool ok;
+};
+
+template <class Tr>
+BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
+  BundleCfg c{};
+  if (K < 1 || K > kBundleMfmaMaxK || F > (1 << 20) || N > (1 << 30) || N < 1) return c;
+  if (cdiv(D, 64) * 2 * nfs_of<Tr>((int)F) * 1024 >= ((int64_t)1 << 31)) return c;
+  c.nt = Tr::kEsz == 2 ? 4 : 2;
+  c.occ = Tr::kEsz == 2 ? 1 : 2;
+  const int nfs = nfs_of<Tr>((int)F);
+  const int pad = Tr::kEsz == 2 ? 8 : 4;
+  const size_t fixed = 16 + sizeof(int) * (32 * c.nt + (size_t)K * kBundleCols);
+  const size_t per_row = (size_t)32 * c.nt * Tr::kEsz;  // bytes per LDS column of the tile
+  // Two workgroups per compute unit (fp32) while the class counters leave
+  // room for a chunk of at least 4 f-steps in half the LDS, else one.
+  if (c.occ > 1 && fixed + per_row * (4 * Tr::kFStep + pad) > (size_t)kLdsBytes / c.occ) c.occ = 1;
+  const size_t budget = (size_t)kLdsBytes / c.occ;
+  if (fixed + per_row * (Tr::kFStep + pad) > budget) return c;
+  int64_t fsc = (int64_t)((budget - fixed) / per_row - pad) / Tr::kFStep;
+  if (fsc > nfs) fsc = nfs;
+  if (fsc < 1) return c;
+  c.fsc = (int)fsc;
+  c.lds = fixed + per_row * (c.fsc * Tr::kFStep + pad);
+  c.ncg = (int)cdiv(cdiv(D, 64), kWaves);
+  const int64_t ntiles = cdiv(N, 32 * c.nt);
+  int64_t g = (int64_t)num_cus() * c.occ / c.ncg;
+  if (g < 1) g = 1;
+  if (g > ntiles) g = ntiles;
+  c.ngroups = (int)g;
+  c.ok = true;
+  return c;
+}
+
 }  // namespace
+
+bool bundle_packed_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  return dt == 0 ? bundle_cfg<TrF32>(N, F, D, K).ok : bundle_cfg<TrBF16>(N, F, D, K).ok;
+}
+
+hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t* y,
+                                int32_t* counts, int64_t N, int64_t F, int64_t D, int64_t K,
+                                int dt, hipStream_t stream) {
+  const dim3 block(kThreads);
+  if (dt == 0) {
+    const BundleCfg c = bundle_cfg<TrF32>(N, F, D, K);
+    if (!c.ok) return hipErrorInvalidValue;
+    const PackGeom g = pack_geom<TrF32>(F, D, 1);
+    auto* k = &bundle_mfma_kernel<TrF32, 2, 2>;
+    const hipError_t a = allow_large_lds<&bundle_mfma_kernel<TrF32, 2, 2>>();
+    if (a != hipSuccess) return a;
+    hipLaunchKernelGGL(k, dim3((unsigned)(c.ncg * c.ngroups)), block, c.lds, stream,
+                       (const float*)X, (const uint4*)packed, y, counts, (int)N, (int)F, (int)D,
+                       (int)K, g.ndb, c.ngroups, c.fsc);
+  } else {
+    const BundleCfg c = bundle_cfg<TrBF16>(N, F, D, K);
+    if (!c.ok) return hipErrorInvalidValue;
+    const PackGeom g = pack_geom<TrBF16>(F, D, 1);
+    auto* k = &bundle_mfma_kernel<TrBF16, 4, 1>;
+    const hipError_t a = allow_large_lds<&bundle_mfma_kernel<TrBF16, 4, 1>>();
+    if (a != hipSuccess) return a;
+    hipLaunchKernelGGL(k, dim3((unsigned)(c.ncg * c.ngroups)), block, c.lds, stream,
+                       (const bf16raw*)X, (const uint4*)packed, y, counts, (int)N, (int)F,
+                       (int)D, (int)K, g.ndb, c.ngroups, c.fsc);
+  }
+  return hipGetLastError();
+}
 
 bool large_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   return dt == 0 ? large_cfg<TrF32>(N, F, D, K).ok : large_cfg<TrBF16>(N, F, D, K).ok;
@@ -1312,7 +1613,7 @@ hipError_t launch_pack(const void* B, const void* C, int64_t F, int64_t D, int64
     hipLaunchKernelGGL(pack_b_f32, dim3((unsigned)((int64_t)g.ndb * g.nfs)), dim3(64), 0, stream,
                        (const float*)B, Bp, (int)F, (int)D, g.ndb, g.nfs);
     hipLaunchKernelGGL(pack_c_f32, dim3((unsigned)((int64_t)g.ndb * g.kb * 4)), dim3(64), 0,
-                       stream, (const float*)C, Cp, (int)D, (int)K, g.ndb, g.kb);
+                       stream, (const float*)C, Cp, (int)D, C ? (int)K : 0, g.ndb, g.kb);
   } else {
     const PackGeom g = pack_geom<TrBF16>(F, D, K);
     uint4* Bp = (uint4*)packed;
@@ -1320,7 +1621,7 @@ hipError_t launch_pack(const void* B, const void* C, int64_t F, int64_t D, int64
     hipLaunchKernelGGL(pack_b_bf16, dim3((unsigned)((int64_t)g.ndb * g.nfs)), dim3(64), 0,
                        stream, (const bf16raw*)B, Bp, (int)F, (int)D, g.ndb, g.nfs);
     hipLaunchKernelGGL(pack_c_bf16, dim3((unsigned)((int64_t)g.ndb * 2 * g.kb)), dim3(64), 0,
-                       stream, (const bf16raw*)C, Cp, (int)D, (int)K, g.ndb, g.kb);
+                       stream, (const bf16raw*)C, Cp, (int)D, C ? (int)K : 0, g.ndb, g.kb);
   }
   return hipGetLastError();
 }

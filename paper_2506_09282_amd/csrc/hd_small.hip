@@ -191,6 +191,12 @@ hipError_t pack_small_t(const void* B, const void* C, int64_t F, int64_t D, int6
   const int64_t gb = cdiv(nblk * F * kW, 256), gc = cdiv(nblk * K * kW, 256);
   hipLaunchKernelGGL(pack_small_kernel<T>, dim3((unsigned)(gb < 65536 ? gb : 65536)), dim3(256), 0,
                      stream, (const T*)B, b, F, D, nblk);
+  if (!C) {
+    // no codebook yet (a model packed for training): class tiles are zero
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_zero(c, (size_t)nblk * K * kW * sizeof(T), stream);
+  }
   hipLaunchKernelGGL(pack_small_kernel<T>, dim3((unsigned)(gc < 65536 ? gc : 65536)), dim3(256), 0,
                      stream, (const T*)C, c, K, D, nblk);
   return hipGetLastError();

@@ -369,13 +369,13 @@ inline void widen_for_final(SmallPlan& p, int64_t N, int64_t K) {
   if (p.lds < want && want <= (size_t)kLdsBudget) p.lds = want;
 }
 
-// Lets kernel k use up to kLdsBudget bytes of dynamic LDS on the current
+// Lets a kernel use up to kLdsBudget bytes of dynamic LDS on the current
 // device (set once per device and kernel).
-template <typename KernelT>
-hipError_t allow_lds(KernelT* k) {
-  static PerDeviceOnce once;
-  return once_per_device(once, [k] {
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+template <auto Kernel>
+hipError_t allow_lds() {
+  static PerDeviceOnce once;  // one per kernel: the template argument is its address
+  return once_per_device(once, [] {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(Kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget);
   });
 }

@@ -267,7 +267,7 @@ __global__ __launch_bounds__(256) void pack_frag_kernel(const float* __restrict_
 
 template <int NTI, int MS>
 hipError_t launch_frag(const SmallPlan& p, const Args& a, const void* frag) {
-  const hipError_t attr = allow_lds(&small_frag_mfma_kernel<NTI, MS>);
+  const hipError_t attr = allow_lds<&small_frag_mfma_kernel<NTI, MS>>();
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((small_frag_mfma_kernel<NTI, MS>), dim3(p.grid), dim3(kFragThreads), p.lds,
                      a.stream, (const float*)a.X, (const float4*)frag, (const float*)a.C,

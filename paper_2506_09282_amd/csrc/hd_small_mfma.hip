@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kThreads) void small_block_mfma_kernel(
 
 template <int NTI, int MS, int LAY>
 hipError_t launch_mfma(const SmallPlan& p, const Args& a) {
-  const hipError_t attr = allow_lds(&small_mfma_kernel<NTI, MS, LAY>);
+  const hipError_t attr = allow_lds<&small_mfma_kernel<NTI, MS, LAY>>();
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((small_mfma_kernel<NTI, MS, LAY>), dim3(p.grid), dim3(kThreads), p.lds,
                      a.stream, (const float*)a.X, (const float*)a.B, (const float*)a.C, a.labels,
@@ -266,7 +266,7 @@ hipError_t launch_mfma_nti(const SmallPlan& p, const Args& a) {
 
 template <int NTI, int MS, int LAY>
 hipError_t launch_bmfma(const SmallPlan& p, const Args& a) {
-  const hipError_t attr = allow_lds(&small_block_mfma_kernel<NTI, MS, LAY>);
+  const hipError_t attr = allow_lds<&small_block_mfma_kernel<NTI, MS, LAY>>();
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((small_block_mfma_kernel<NTI, MS, LAY>), dim3(p.grid), dim3(kThreads), p.lds,
                      a.stream, (const float*)a.X, (const float*)a.B, (const float*)a.C, a.labels,

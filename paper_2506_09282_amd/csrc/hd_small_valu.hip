@@ -151,7 +151,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
 
 template <typename T, int NB, int LAY>
 hipError_t launch_valu(const SmallPlan& p, const Args& a) {
-  const hipError_t attr = allow_lds(&small_valu_kernel<T, NB, LAY>);
+  const hipError_t attr = allow_lds<&small_valu_kernel<T, NB, LAY>>();
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((small_valu_kernel<T, NB, LAY>), dim3(p.grid), dim3(kThreads), p.lds,
                      a.stream, (const T*)a.X, (const T*)a.B, (const T*)a.C, a.labels, a.scores,

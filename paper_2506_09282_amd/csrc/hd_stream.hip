@@ -434,7 +434,7 @@ __global__ __launch_bounds__(kStreamThreads, 1) void stream_frag_kernel(
 
 template <int NTI, int MS>
 hipError_t launch_stream_t(const SmallPlan& p, const StreamArgs& a) {
-  const hipError_t attr = allow_lds(&stream_frag_kernel<NTI, MS>);
+  const hipError_t attr = allow_lds<&stream_frag_kernel<NTI, MS>>();
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((stream_frag_kernel<NTI, MS>), dim3(p.grid + 1), dim3(kStreamThreads), p.lds,
                      a.stream, (const float*)a.X, (const float4*)a.frag, (const float*)a.C,

@@ -170,3 +170,15 @@ def test_training_argument_errors(L):
     assert g(FAKE, FAKE, 0, 64, None) == hd.HD_ERR_ARG
     assert g(FAKE, FAKE, 3, 0, None) == hd.HD_ERR_ARG
     assert g(FAKE + 1, FAKE, 3, 64, None) == hd.HD_ERR_ARG
+
+
+def test_packed_training_argument_errors(L):
+    f = L.hd_bundle_classes_packed
+    assert f(FAKE, FAKE, FAKE, FAKE, 0, 8, 64, 3, 0, None) == hd.HD_OK
+    assert f(None, FAKE, FAKE, FAKE, 4, 8, 64, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, None, FAKE, FAKE, 4, 8, 64, 3, 0, None) == hd.HD_ERR_ARG
+    assert f(FAKE, FAKE + 16, FAKE, FAKE, 4, 8, 64, 3, 0, None) == hd.HD_ERR_ARG  # image alignment
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 8, 64, 129, 0, None) == hd.HD_ERR_UNSUPPORTED
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 8, 64, 3, 5, None) == hd.HD_ERR_ARG
+    # a model packed without a codebook: C may be NULL, B may not
+    assert L.hd_pack_model(None, None, 8, 16, 3, 0, FAKE, 1 << 30, None) == hd.HD_ERR_ARG

@@ -39,17 +39,25 @@ def labels_for(N, K, seed, spill=0):
     return y
 
 
-def gpu_train(hd, X, B, y, K, dtype, chunks=1):
+PATHS = ["raw", "packed"]
+
+
+def gpu_train(hd, X, B, y, K, dtype, chunks=1, path="raw"):
+    """Class counts and codebook from the GPU: ``raw`` is hd_bundle_classes
+    (B as given), ``packed`` hd_bundle_classes_packed (B tiled once by
+    hd_pack_model with no codebook)."""
     torch = torch_or_skip()
     Xd, Bd = dev(X, dtype), dev(B, dtype)
     yd = torch.from_numpy(np.ascontiguousarray(y, np.int32)).cuda()
-    counts = None
+    model = hd.pack_model(Bd) if path == "packed" else None
+    counts = torch.zeros((K, B.shape[1]), dtype=torch.int32, device="cuda")
     N = X.shape[0]
     cuts = np.linspace(0, N, chunks + 1).astype(int)
     for a, b in zip(cuts[:-1], cuts[1:]):
-        if counts is None:
-            counts = torch.zeros((K, B.shape[1]), dtype=torch.int32, device="cuda")
-        hd.bundle_classes(Xd[a:b], Bd, yd[a:b], K, counts=counts)
+        if model is not None:
+            hd.bundle_classes_packed(Xd[a:b], model, yd[a:b], K, counts=counts)
+        else:
+            hd.bundle_classes(Xd[a:b], Bd, yd[a:b], K, counts=counts)
     M = hd.class_hardsign(counts)
     torch.cuda.synchronize()
     return counts.cpu().numpy().astype(np.int64), M.cpu().numpy().astype(np.float64)
@@ -91,32 +99,38 @@ INTEGER = [
     (130, 3072, 1024, 100, 3),
     (50, 40, 300, 80, 0),
     (2100, 33, 640, 512, 40),
+    (3000, 100, 2100, 128, 40),
+    (4100, 2999, 1000, 7, 0),
 ]
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("N,F,D,K,spill", INTEGER)
-def test_integer_counts_bit_exact(hd, N, F, D, K, spill, dtype):
-    announce(f"train integer {dtype} N={N} F={F} D={D} K={K} spill={spill}")
+def test_integer_counts_bit_exact(hd, N, F, D, K, spill, dtype, path):
+    if path == "packed" and K > 128:
+        pytest.skip("the packed (matrix-core) path takes K <= 128")
+    announce(f"train integer {path} {dtype} N={N} F={F} D={D} K={K} spill={spill}")
     X, B, _ = hd_inputs.make_integer_inputs(N, F, D, 1, seed=N + F + K)
     y = labels_for(N, K, N + K, spill)
     ref = oracle.bundle(X, B, y, K)
-    counts, M = gpu_train(hd, X, B, y, K, dtype)
+    counts, M = gpu_train(hd, X, B, y, K, dtype, path=path)
     check_exact(counts, M, ref)
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_zero_sums_and_tied_counts(hd, dtype):
+def test_zero_sums_and_tied_counts(hd, dtype, path):
     """X and B in {-1, 0, 1}: many encoding sums are exactly 0 (HardSign gives
     +1) and many class counts are exactly 0 (the codebook gives +1)."""
     N, F, D, K = 700, 40, 1000, 9
-    announce(f"train ties {dtype} N={N} F={F} D={D} K={K}")
+    announce(f"train ties {path} {dtype} N={N} F={F} D={D} K={K}")
     X, B, _ = hd_inputs.make_integer_inputs(N, F, D, 1, seed=5, x_range=1, b_range=1)
     y = labels_for(N, K, 5)
     y[y == 4] = 3  # class 4 is empty: all +1
     ref = oracle.bundle(X, B, y, K)
     assert (ref["counts"] == 0).sum() > 100
-    counts, M = gpu_train(hd, X, B, y, K, dtype)
+    counts, M = gpu_train(hd, X, B, y, K, dtype, path=path)
     check_exact(counts, M, ref)
     assert np.all(M[4] == 1.0) and np.all(counts[4] == 0)
 
@@ -132,27 +146,29 @@ REAL = [
 ]
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("name,N,F,D,K,dist,dtype", REAL)
-def test_real_inputs_within_fragile_flips(hd, name, N, F, D, K, dist, dtype):
-    announce(f"train real {name} {dtype} N={N} F={F} D={D} K={K}")
+def test_real_inputs_within_fragile_flips(hd, name, N, F, D, K, dist, dtype, path):
+    announce(f"train real {path} {name} {dtype} N={N} F={F} D={D} K={K}")
     X, B, _ = hd_inputs.make_inputs(N, F, D, 1, dist, seed=3, dtype=dtype)
     y = labels_for(N, K, 3)
     ref = oracle.bundle(X, B, y, K)
-    counts, M = gpu_train(hd, X, B, y, K, dtype)
+    counts, M = gpu_train(hd, X, B, y, K, dtype, path=path)
     ndiff = check_fragile(counts, M, X, B, y, K, ref)
-    print(f"[train] {name}: {ndiff} of {counts.size} counts differ (fragile samples)")
+    print(f"[train] {path} {name}: {ndiff} of {counts.size} counts differ (fragile samples)")
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("chunks", [2, 7])
-def test_chunked_accumulation_equals_one_call(hd, chunks):
+def test_chunked_accumulation_equals_one_call(hd, chunks, path):
     """Counts are integers added with atomics: feeding the samples in chunks
     gives the same counts bit for bit, on real-valued inputs too."""
     N, F, D, K = 1300, 561, 2048, 6
-    announce(f"train chunks={chunks} N={N}")
+    announce(f"train chunks={chunks} {path} N={N}")
     X, B, _ = hd_inputs.make_inputs(N, F, D, 1, "uniform_pm1", seed=9)
     y = labels_for(N, K, 9)
-    c1, m1 = gpu_train(hd, X, B, y, K, "f32", chunks=1)
-    ck, mk = gpu_train(hd, X, B, y, K, "f32", chunks=chunks)
+    c1, m1 = gpu_train(hd, X, B, y, K, "f32", chunks=1, path=path)
+    ck, mk = gpu_train(hd, X, B, y, K, "f32", chunks=chunks, path=path)
     assert np.array_equal(c1, ck)
     assert np.array_equal(m1, mk)
 
@@ -164,8 +180,24 @@ def test_empty_batch_leaves_counts(hd):
     B = torch.ones((5, 64), dtype=torch.float32, device="cuda")
     y = torch.empty((0,), dtype=torch.int32, device="cuda")
     hd.bundle_classes(X, B, y, 3, counts=counts)
+    hd.bundle_classes_packed(X, hd.pack_model(B), y, 3, counts=counts)
     torch.cuda.synchronize()
     assert bool((counts == 7).all())
+
+
+def test_packed_model_with_codebook_trains_the_same(hd):
+    """The packed path reads only the tiled B: a model packed with a codebook
+    trains exactly like one packed without."""
+    torch = torch_or_skip()
+    N, F, D, K = 500, 300, 1000, 5
+    X, B, C = hd_inputs.make_inputs(N, F, D, K, "uniform_pm1", seed=12)
+    y = labels_for(N, K, 12)
+    Xd, Bd, Cd = dev(X, "f32"), dev(B, "f32"), dev(C, "f32")
+    yd = torch.from_numpy(y).cuda()
+    a = hd.bundle_classes_packed(Xd, hd.pack_model(Bd), yd, K)
+    b = hd.bundle_classes_packed(Xd, hd.pack_model(Bd, Cd), yd, K)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
 
 
 def test_single_sample_classes_round_trip(hd):
@@ -178,13 +210,15 @@ def test_single_sample_classes_round_trip(hd):
     announce(f"train round trip K={K} F={F} D={D}")
     X, B, _ = hd_inputs.make_integer_inputs(K, F, D, 1, seed=4)
     y = np.arange(K, dtype=np.int32)[::-1].copy()
-    counts, M = gpu_train(hd, X, B, y, K, "f32")
     H = oracle.encode(X, B)["H"]
-    assert np.array_equal(M[y], H)
-    Xd = dev(X, "f32")
-    Md = torch.from_numpy(M.astype(np.float32)).cuda()
-    labels, S = hd.infer(Xd, dev(B, "f32"), Md, return_scores=True)
-    torch.cuda.synchronize()
-    S = S.cpu().numpy()
-    assert np.array_equal(labels.cpu().numpy(), y)
-    assert np.all(S[np.arange(K), y] == D)
+    for path in PATHS:
+        counts, M = gpu_train(hd, X, B, y, K, "f32", path=path)
+        assert np.array_equal(M[y], H)
+        Xd, Bd = dev(X, "f32"), dev(B, "f32")
+        Md = torch.from_numpy(M.astype(np.float32)).cuda()
+        for labels, S in (hd.infer(Xd, Bd, Md, return_scores=True),
+                          hd.infer_packed(Xd, hd.pack_model(Bd, Md), return_scores=True)):
+            torch.cuda.synchronize()
+            S = S.cpu().numpy()
+            assert np.array_equal(labels.cpu().numpy(), y)
+            assert np.all(S[np.arange(K), y] == D)
