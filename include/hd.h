@@ -243,6 +243,14 @@ hd_status hd_bundle_classes_packed(const void *X, const void *packed, const int3
                                    hd_dtype dt, hipStream_t stream);
 
 /*
+ * Introspection: the name of the kernel that hd_bundle_classes (packed == 0)
+ * or hd_bundle_classes_packed (packed != 0) launches for these sizes,
+ * assuming a 16-byte aligned X; "" when the call would be rejected. Static
+ * string.
+ */
+const char *hd_bundle_kernel(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, int packed);
+
+/*
  * Introspection: the name of the main kernel that hd_infer (packed == 0) or
  * hd_infer_packed (packed != 0) launches for these sizes, assuming 16-byte
  * aligned operands; "" when the call would be rejected. The returned string

@@ -40,6 +40,7 @@ SYMBOLS = (
     "hd_bundle_classes",
     "hd_class_hardsign",
     "hd_bundle_classes_packed",
+    "hd_bundle_kernel",
 )
 
 _lib = None
@@ -102,6 +103,8 @@ def lib():
         L.hd_class_hardsign.restype = i32
         L.hd_bundle_classes_packed.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp]
         L.hd_bundle_classes_packed.restype = i32
+        L.hd_bundle_kernel.argtypes = [i64, i64, i64, i64, i32, i32]
+        L.hd_bundle_kernel.restype = ctypes.c_char_p
         _lib = L
         return L
 
@@ -424,6 +427,13 @@ def bundle_classes_packed(X, model: PackedModel, y, K: int, counts=None):
                                         _stream_ptr(X.device))
     _raise(st, "hd_bundle_classes_packed")
     return counts
+
+
+def bundle_kernel(N: int, F: int, D: int, K: int, dtype, packed: bool = True) -> str:
+    """Name of the kernel bundle_classes(_packed) launches for these sizes."""
+    torch = _torch()
+    dt = HD_F32 if dtype == torch.float32 else HD_BF16
+    return lib().hd_bundle_kernel(N, F, D, K, dt, 1 if packed else 0).decode()
 
 
 def class_hardsign(counts, out=None):

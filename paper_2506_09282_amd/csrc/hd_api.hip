@@ -302,6 +302,12 @@ hd_status hd_bundle_classes_packed(const void* X, const void* packed, const int3
   return from_hip(hd::launch_bundle_packed(X, packed, y, counts, N, F, D, K, dt, stream));
 }
 
+const char* hd_bundle_kernel(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, int packed) {
+  if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return "";
+  if (packed) return hd::bundle_packed_kernel_name(N, F, D, K, dt);
+  return hd::bundle_supported(K) ? "bundle_valu_kernel" : "";
+}
+
 hd_status hd_class_hardsign(const int32_t* counts, float* M, int64_t K, int64_t D,
                             hipStream_t stream) {
   if (K < 1 || D < 1) return HD_ERR_ARG;

@@ -82,6 +82,8 @@ hipError_t launch_class_hardsign(const int32_t* counts, float* M, int64_t K, int
 // (the large-batch section at the start of the image).
 constexpr int64_t kBundleMfmaMaxK = 128;
 bool bundle_packed_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
+// Name of the kernel launch_bundle_packed uses for 16-byte aligned X ("" if unsupported).
+const char* bundle_packed_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
 hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t* y,
                                 int32_t* counts, int64_t N, int64_t F, int64_t D, int64_t K,
                                 int dt, hipStream_t stream);

@@ -1345,6 +1345,217 @@ __global__ __launch_bounds__(kThreads, OCC) void bundle_mfma_kernel(
   }
 }
 
+// bf16 training with the X chunks double-buffered in LDS and filled by
+// buffer-to-LDS loads, on the schedule of large_chunked_dma_kernel: 64-sample
+// tiles, chunks of kDmaFsc f-steps, the next chunk's loads issued two per
+// f-step at the start of the current one, the B fragment ring running on
+// across chunks and tiles (a wave keeps its units for every tile). The
+// labels of the tile a chunk belongs to travel with it: one 4-byte
+// buffer-to-LDS load per wave at the chunk's first step (every wave writes the
+// same values) into a label buffer selected by tile parity.
+// Requires F % 8 == 0 and a 16-byte aligned X.
+template <int UPW>
+__global__ __launch_bounds__(kThreads, 1) void bundle_dma_kernel(
+    const bf16raw* __restrict__ X, const uint4* __restrict__ Bp, const int32_t* __restrict__ y,
+    int32_t* __restrict__ counts, int N, int F, int D, int K, int ndb, int ngroups) {
+  typedef TrBF16 Tr;
+  constexpr int NTILES = kDmaNtiles;
+  constexpr int NT = 32 * NTILES;
+  constexpr int kPF = UPW > 1 ? 4 : prefetch_of(NTILES, 1);
+  constexpr int FSC = kDmaFsc;
+  constexpr int W = 2 * FSC + 1;                 // 16-byte slots per LDS row
+  constexpr int pitch = 8 * W;                   // elements
+  constexpr int P = dma_loads_per_wave(NTILES);  // X loads per wave per chunk
+  constexpr int kDmaSteps = (P + 1) / 2;
+  constexpr int kAfter = 2 * UPW * (FSC - kDmaSteps);
+  constexpr int kWait = kAfter < 2 * UPW * kPF ? kAfter : 2 * UPW * kPF;
+  constexpr int buf_elems = P * kThreads * 8;
+  constexpr int kCols = kWaves * UPW * 64;  // columns per workgroup
+  static_assert(NT == 64 && FSC % kPF == 0 && kDmaSteps <= FSC && kWait <= 63, "schedule");
+  constexpr int kWaitImm = 0x0F70 | (kWait & 15) | ((kWait >> 4) << 14);
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nfs = nfs_of<Tr>(F);
+  const int nchunks = (nfs + FSC - 1) / FSC;
+  const int nfl = nchunks * FSC;
+  const int units = ndb / 2;
+  const int ncg = (units + kWaves * UPW - 1) / (kWaves * UPW);
+  const int cg = blockIdx.x % ncg;
+  const int sg = blockIdx.x / ncg;
+  const int ntiles = (N + NT - 1) / NT;
+  const int t_begin = (int)((int64_t)ntiles * sg / ngroups);
+  const int t_end = (int)((int64_t)ntiles * (sg + 1) / ngroups);
+
+  // LDS: [two X buffers | zero slot | labels 2 x NT | counters K x kCols]
+  bf16raw* xb = reinterpret_cast<bf16raw*>(lds);
+  const bf16raw* xzero = xb + 2 * buf_elems;
+  int* ys = reinterpret_cast<int*>(xb + 2 * buf_elems + 8);
+  int* cnt = ys + 2 * NT;
+  if (tid == 0) *reinterpret_cast<uint4*>(xb + 2 * buf_elems) = make_uint4(0u, 0u, 0u, 0u);
+  for (int i = tid; i < K * kCols; i += kThreads) cnt[i] = 0;
+
+  // Load p of this wave for chunk ch of tile tl into buffer buf (rows past N
+  // and columns past F are out of the resource's range and read as zero).
+  auto dma = [&](int tl, int ch, int p, int buf) {
+    const int64_t n0 = (int64_t)tl * NT;
+    const int rows = (int)min((int64_t)NT, (int64_t)N - n0);
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16raw*>(X + n0 * F), 0, rows * F * 2, 0x00020000);
+    int q = (p * kWaves + wave) * 64 + lane;
+    asm volatile("" : "+v"(q));
+    const int r = q / W, rem = q - r * W;
+    const int col = (ch * FSC + (rem >> 1)) * 16 + (rem & 1) * 8;
+    const bool ok = r < rows && rem < 2 * FSC && col < F;
+    const unsigned off = ok ? (unsigned)((r * F + col) * 2) : 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        xr,
+        (__attribute__((address_space(3))) void*)(xb + buf * buf_elems +
+                                                  (p * kWaves + wave) * 64 * 8),
+        16, off, 0, 0, 0);
+  };
+  // The labels of tile tl into label buffer tl & 1 (lane l: row l).
+  auto label_dma = [&](int tl) {
+    const int64_t n0 = (int64_t)tl * NT;
+    const int rows = (int)min((int64_t)NT, (int64_t)N - n0);
+    const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t*>(y + n0), 0, rows * 4, 0x00020000);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        yr, (__attribute__((address_space(3))) void*)(ys + (tl & 1) * NT), 4,
+        (unsigned)lane * 4u, 0, 0, 0);
+  };
+
+  const int xrow = lane & 31, xhalf = lane >> 5;
+  const int xlane = xrow * pitch + xhalf * (Tr::kFStep / 2);
+  const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(Bp), 0, ndb * nfs * 1024, 0x00020000);
+  auto bfrag = [&](int uu, int fs, int b) -> uint4 {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         brsrc, ((2 * uu + b) * nfs + fs) * 1024 + lane * 16, 0, 0));
+  };
+  // this wave's j-th unit (a valid unit of the group when it has none:
+  // computed and discarded)
+  int uu[UPW];
+  bool uvalid[UPW];
+#pragma unroll
+  for (int j = 0; j < UPW; ++j) {
+    const int u = cg * kWaves * UPW + j * kWaves + wave;
+    uvalid[j] = u < units;
+    uu[j] = uvalid[j] ? u : cg * kWaves * UPW;
+  }
+
+  if (t_begin < t_end) {
+    label_dma(t_begin);
+    for (int p = 0; p < P; ++p) dma(t_begin, 0, p, 0);
+  }
+  uint4 afr[UPW][kPF][2];
+#pragma unroll
+  for (int j = 0; j < UPW; ++j)
+#pragma unroll
+    for (int i = 0; i < kPF; ++i) {
+      afr[j][i][0] = bfrag(uu[j], i < nfs ? i : nfs - 1, 0);
+      afr[j][i][1] = bfrag(uu[j], i < nfs ? i : nfs - 1, 1);
+    }
+  int cur = 0;
+  for (int tile = t_begin; tile < t_end; ++tile) {
+    const int rows = min(NT, N - tile * NT);
+    f32x16 vacc[UPW][2][NTILES];
+#pragma unroll
+    for (int j = 0; j < UPW; ++j)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) vacc[j][b][t][r] = 0.0f;
+
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const int fs0 = ch * FSC;
+      const int fsn = min(FSC, nfs - fs0);
+      // the chunk to fill next: the next one of this tile, else the first of
+      // the next tile (the last tile reloads its own first chunk, unread)
+      const bool last = ch + 1 == nchunks;
+      const int ntl = last ? (tile + 1 < t_end ? tile + 1 : tile) : tile;
+      const int nch = last ? 0 : ch + 1;
+      __builtin_amdgcn_s_waitcnt(kWaitImm);
+      __syncthreads();
+      const uint32_t xc = lds_addr(xb + cur * buf_elems + xlane);
+      const uint32_t xz = lds_addr(xzero);
+      const int nbuf = cur ^ 1;
+      uint4 xfr[2][NTILES];
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t) xfr[0][t] = lds_read16_issue(xc + t * 64 * pitch);
+#pragma unroll
+      for (int s = 0; s < FSC; ++s) {
+        const int i = s % kPF;
+        lds_reads_complete<NTILES>(xfr[s & 1]);
+#pragma unroll
+        for (int t = 0; t < NTILES; ++t)
+          xfr[(s + 1) & 1][t] =
+              lds_read16_issue(s + 1 < fsn ? xc + t * 64 * pitch + (s + 1) * 32 : xz);
+#pragma unroll
+        for (int j = 0; j < UPW; ++j)
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int t = 0; t < NTILES; ++t)
+              Tr::stage1(vacc[j][b][t], xfr[s & 1][t], afr[j][i][b]);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NTILES * UPW, 0);
+        if (s == 0)
+          __builtin_amdgcn_sched_group_barrier(0x020, 2 * UPW + 3, 0);
+        else if (s < kDmaSteps)
+          __builtin_amdgcn_sched_group_barrier(0x020, 2 * UPW + 2, 0);
+        else
+          __builtin_amdgcn_sched_group_barrier(0x020, 2 * UPW, 0);
+        // refill: f-step g of the units (past the padded end: the next tile's
+        // first steps of the same units)
+        const int g = fs0 + s + kPF;
+        const int rg0 = g < nfl ? g : g - nfl;
+        const int rg = rg0 < nfs ? rg0 : nfs - 1;
+#pragma unroll
+        for (int j = 0; j < UPW; ++j) {
+          afr[j][i][0] = bfrag(uu[j], rg, 0);
+          afr[j][i][1] = bfrag(uu[j], rg, 1);
+        }
+        if (s == 0) label_dma(ntl);  // before this chunk's last X load
+        if (s < kDmaSteps) {
+          dma(ntl, nch, 2 * s < P ? 2 * s : P - 1, nbuf);
+          dma(ntl, nch, 2 * s + 1 < P ? 2 * s + 1 : P - 1, nbuf);
+        }
+      }
+      lds_reads_complete<NTILES>(xfr[FSC & 1]);
+      cur = nbuf;
+    }
+    // HardSign (Eq. 1) and the class sums of this tile.
+    const int* yt = ys + (tile & 1) * NT;
+#pragma unroll
+    for (int j = 0; j < UPW; ++j) {
+      if (!uvalid[j]) continue;
+#pragma unroll
+      for (int t = 0; t < NTILES; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = 32 * t + 8 * (r >> 2) + 4 * xhalf + (r & 3);
+          const int k = row < rows ? yt[row] : -1;
+          if (k >= 0 && k < K) {
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+              atomicAdd(&cnt[k * kCols + (j * kWaves + wave) * 64 + 32 * b + xrow],
+                        vacc[j][b][t][r] >= 0.0f ? 1 : -1);
+          }
+        }
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // no load into LDS is still in flight
+  __syncthreads();
+  const int64_t d0 = (int64_t)cg * kCols;
+  for (int i = tid; i < K * kCols; i += kThreads) {
+    const int k = i / kCols, c = i % kCols;
+    const int v = cnt[i];
+    if (v != 0 && d0 + c < D) atomicAdd(&counts[(int64_t)k * D + d0 + c], v);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Host-side configuration.
 // ---------------------------------------------------------------------------
@@ -1502,15 +1713,39 @@ hipError_t launch_tr(const void* X, const void* packed, int32_t* labels, float* 
 // number of sample-tile groups.
 struct BundleCfg {
   int nt, occ, fsc, ngroups, ncg;
+  int dma_upw;  // > 0: the double-buffered bf16 kernel with this many units per wave
   size_t lds;
   bool ok;
 };
 
 template <class Tr>
-BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K) {
+BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) {
   BundleCfg c{};
   if (K < 1 || K > kBundleMfmaMaxK || F > (1 << 20) || N > (1 << 30) || N < 1) return c;
   if (cdiv(D, 64) * 2 * nfs_of<Tr>((int)F) * 1024 >= ((int64_t)1 << 31)) return c;
+  if (Tr::kEsz == 2 && F % 8 == 0 && x16) {
+    // double-buffered kernel: two units per wave while the class counters fit
+    const size_t base = (size_t)2 * dma_loads_per_wave(kDmaNtiles) * kThreads * 16 + 16 +
+                        sizeof(int) * 2 * 32 * kDmaNtiles;
+    for (int upw : {2, 1}) {
+      const size_t need = base + sizeof(int) * (size_t)K * kWaves * upw * 64;
+      if (need <= (size_t)kLdsBytes) {
+        c.dma_upw = upw;
+        c.nt = kDmaNtiles;
+        c.occ = 1;
+        c.fsc = kDmaFsc;
+        c.lds = need;
+        c.ncg = (int)cdiv(cdiv(D, 64), kWaves * upw);
+        const int64_t ntiles = cdiv(N, 32 * c.nt);
+        int64_t g = (int64_t)num_cus() / c.ncg;
+        if (g < 1) g = 1;
+        if (g > ntiles) g = ntiles;
+        c.ngroups = (int)g;
+        c.ok = true;
+        return c;
+      }
+    }
+  }
   c.nt = Tr::kEsz == 2 ? 4 : 2;
   c.occ = Tr::kEsz == 2 ? 1 : 2;
   const int nfs = nfs_of<Tr>((int)F);
@@ -1543,6 +1778,13 @@ bool bundle_packed_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt)
   return dt == 0 ? bundle_cfg<TrF32>(N, F, D, K).ok : bundle_cfg<TrBF16>(N, F, D, K).ok;
 }
 
+const char* bundle_packed_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  if (dt == 0) return bundle_cfg<TrF32>(N, F, D, K).ok ? "bundle_mfma_kernel" : "";
+  const BundleCfg c = bundle_cfg<TrBF16>(N, F, D, K);
+  if (!c.ok) return "";
+  return c.dma_upw > 0 ? "bundle_dma_kernel" : "bundle_mfma_kernel";
+}
+
 hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t* y,
                                 int32_t* counts, int64_t N, int64_t F, int64_t D, int64_t K,
                                 int dt, hipStream_t stream) {
@@ -1558,9 +1800,26 @@ hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t
                        (const float*)X, (const uint4*)packed, y, counts, (int)N, (int)F, (int)D,
                        (int)K, g.ndb, c.ngroups, c.fsc);
   } else {
-    const BundleCfg c = bundle_cfg<TrBF16>(N, F, D, K);
+    const BundleCfg c = bundle_cfg<TrBF16>(N, F, D, K, ((uintptr_t)X % 16) == 0);
     if (!c.ok) return hipErrorInvalidValue;
     const PackGeom g = pack_geom<TrBF16>(F, D, 1);
+    if (c.dma_upw > 0) {
+      const dim3 grid((unsigned)(c.ncg * c.ngroups));
+      if (c.dma_upw == 2) {
+        const hipError_t a = allow_large_lds<&bundle_dma_kernel<2>>();
+        if (a != hipSuccess) return a;
+        hipLaunchKernelGGL(bundle_dma_kernel<2>, grid, block, c.lds, stream, (const bf16raw*)X,
+                           (const uint4*)packed, y, counts, (int)N, (int)F, (int)D, (int)K,
+                           g.ndb, c.ngroups);
+      } else {
+        const hipError_t a = allow_large_lds<&bundle_dma_kernel<1>>();
+        if (a != hipSuccess) return a;
+        hipLaunchKernelGGL(bundle_dma_kernel<1>, grid, block, c.lds, stream, (const bf16raw*)X,
+                           (const uint4*)packed, y, counts, (int)N, (int)F, (int)D, (int)K,
+                           g.ndb, c.ngroups);
+      }
+      return hipGetLastError();
+    }
     auto* k = &bundle_mfma_kernel<TrBF16, 4, 1>;
     const hipError_t a = allow_large_lds<&bundle_mfma_kernel<TrBF16, 4, 1>>();
     if (a != hipSuccess) return a;

@@ -5,7 +5,7 @@
 //   M[k,d]       = HardSign(counts[k,d])          (Eq. 1: ties and empty classes to +1)
 // (encoding Eq. 2-3, bundling Sec. II-A). The sums are exact integers.
 //
-// bundle_kernel: one workgroup per (64-column block of D, share of the
+// bundle_valu_kernel: one workgroup per (64-column block of D, share of the
 // samples). It encodes 64-sample x 64-column tiles (F streamed through LDS in
 // steps of 16, a 4x4 register tile per thread, fp32 accumulation), applies
 // HardSign, adds each +1/-1 into its class's counter in LDS (integer atomics),
@@ -23,7 +23,7 @@ constexpr int kTile = 64;     // samples and columns per tile
 constexpr int kFStep = 16;    // features per LDS step
 
 template <typename T>
-__global__ __launch_bounds__(256) void bundle_kernel(const T* __restrict__ X,
+__global__ __launch_bounds__(256) void bundle_valu_kernel(const T* __restrict__ X,
                                                      const T* __restrict__ B,
                                                      const int32_t* __restrict__ y,
                                                      int32_t* __restrict__ counts, int64_t N,
@@ -112,7 +112,7 @@ template <typename T>
 hipError_t allow_counter_lds() {
   static PerDeviceOnce once;
   return once_per_device(once, [] {
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(&bundle_kernel<T>),
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&bundle_valu_kernel<T>),
                                hipFuncAttributeMaxDynamicSharedMemorySize,
                                (int)(sizeof(int) * kBundleMaxK * kTile));
   });
@@ -136,10 +136,10 @@ hipError_t launch_bundle(const void* X, const void* B, const int32_t* y, int32_t
   const hipError_t attr = dt == 0 ? allow_counter_lds<float>() : allow_counter_lds<bf16raw>();
   if (attr != hipSuccess) return attr;
   if (dt == 0)
-    hipLaunchKernelGGL(bundle_kernel<float>, grid, block, lds, stream, (const float*)X,
+    hipLaunchKernelGGL(bundle_valu_kernel<float>, grid, block, lds, stream, (const float*)X,
                        (const float*)B, y, counts, N, F, D, (int)K, (int)nsplit);
   else
-    hipLaunchKernelGGL(bundle_kernel<bf16raw>, grid, block, lds, stream, (const bf16raw*)X,
+    hipLaunchKernelGGL(bundle_valu_kernel<bf16raw>, grid, block, lds, stream, (const bf16raw*)X,
                        (const bf16raw*)B, y, counts, N, F, D, (int)K, (int)nsplit);
   return hipGetLastError();
 }

@@ -118,6 +118,36 @@ def test_integer_counts_bit_exact(hd, N, F, D, K, spill, dtype, path):
     check_exact(counts, M, ref)
 
 
+# Every training kernel on integer inputs, asserting which one ran:
+# (N, F, D, K, dtype, path, kernel).
+KERNELS = [
+    (700, 100, 1000, 9, "f32", "raw", "bundle_valu_kernel"),
+    (700, 100, 1000, 9, "bf16", "raw", "bundle_valu_kernel"),
+    (700, 100, 1000, 9, "f32", "packed", "bundle_mfma_kernel"),
+    (3000, 2999, 700, 100, "f32", "packed", "bundle_mfma_kernel"),
+    (700, 101, 1000, 9, "bf16", "packed", "bundle_mfma_kernel"),
+    (130, 3072, 1024, 100, "bf16", "packed", "bundle_mfma_kernel"),
+    (1000, 3072, 2048, 10, "bf16", "packed", "bundle_dma_kernel"),
+    (1, 3072, 2048, 10, "bf16", "packed", "bundle_dma_kernel"),
+    (65, 256, 10240, 26, "bf16", "packed", "bundle_dma_kernel"),
+    (2047, 616, 1000, 60, "bf16", "packed", "bundle_dma_kernel"),
+    (333, 8, 64, 2, "bf16", "packed", "bundle_dma_kernel"),
+]
+
+
+@pytest.mark.parametrize("N,F,D,K,dtype,path,kernel", KERNELS)
+def test_every_training_kernel_bit_exact(hd, N, F, D, K, dtype, path, kernel):
+    torch = torch_or_skip()
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    assert hd.bundle_kernel(N, F, D, K, tdt, packed=(path == "packed")) == kernel
+    announce(f"train kernel {kernel} {dtype} N={N} F={F} D={D} K={K}")
+    X, B, _ = hd_inputs.make_integer_inputs(N, F, D, 1, seed=N + 3 * F + K)
+    y = labels_for(N, K, N + F, spill=N // 50)
+    ref = oracle.bundle(X, B, y, K)
+    counts, M = gpu_train(hd, X, B, y, K, dtype, path=path)
+    check_exact(counts, M, ref)
+
+
 @pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_zero_sums_and_tied_counts(hd, dtype, path):
@@ -139,6 +169,7 @@ def test_zero_sums_and_tied_counts(hd, dtype, path):
 # classes), with a few thousand samples.
 REAL = [
     ("activity", 2000, 561, 10240, 6, "uniform_pm1", "f32"),
+    ("colour_dma", 1200, 3072, 4096, 10, "uniform01", "bf16"),
     ("image", 1500, 617, 10240, 26, "uniform01", "f32"),
     ("image", 1500, 617, 10240, 26, "uniform01", "bf16"),
     ("colour", 600, 3072, 4096, 10, "uniform01", "bf16"),
