@@ -158,3 +158,14 @@ def make_integer_inputs(N: int, F: int, D: int, K: int, seed: int = 0,
     B = gB.integers(-b_range, b_range + 1, (F, D)).astype(np.float32)
     C = gC.integers(-c_range, c_range + 1, (K, D)).astype(np.float32)
     return np.ascontiguousarray(X), np.ascontiguousarray(B), np.ascontiguousarray(C)
+
+
+def make_int8_inputs(N: int, F: int, D: int, K: int, seed: int = 0, lo: int = -128,
+                     hi: int = 127):
+    """int8 inputs X[N, F], B[F, D], C[K, D] ~ U{lo..hi} (the int8 model
+    variant); returned as int8 arrays."""
+    gX, gB, gC = _generators(seed)
+    X = gX.integers(lo, hi + 1, (N, F)).astype(np.int8)
+    B = gB.integers(lo, hi + 1, (F, D)).astype(np.int8)
+    C = gC.integers(lo, hi + 1, (K, D)).astype(np.int8)
+    return np.ascontiguousarray(X), np.ascontiguousarray(B), np.ascontiguousarray(C)

@@ -1,6 +1,6 @@
 /*
  * hd.h — C ABI of the MI355X (gfx950) batched hyperdimensional-computing
- * inference library.
+ * inference library (with single-pass training and an int8 model variant).
  *
  * The operation is the two-stage HDC inference of ScalableHD (Sec. II-D,
  * Alg. 1): with raw features X[N,F], base hypervectors B[F,D] and class
@@ -12,8 +12,8 @@
  *   - Layout: dense, contiguous, row-major. X[N,F], B[F,D], C[K,D], H[N,D],
  *     scores[N,K]. The paper's J = M^T is C read column-major.
  *   - Types: hd_dtype names the element type of X, B and C (HD_BF16 buffers
- *     hold raw bfloat16 bit patterns). Accumulation is always fp32. H and
- *     scores are fp32; labels are int32 in [0, K).
+ *     hold raw bfloat16 bit patterns). Accumulation is fp32 (int32 for
+ *     HD_I8 Stage I). H and scores are fp32; labels are int32 in [0, K).
  *   - Pointers: X, B, C, H, labels, scores, workspace and packed models are
  *     DEVICE pointers owned by the caller. The library allocates nothing,
  *     frees nothing and keeps no pointer after a call returns. Outputs must
@@ -60,7 +60,22 @@ typedef enum {
   HD_ERR_HIP = 4          /* a HIP launch failed */
 } hd_status;
 
-typedef enum { HD_F32 = 0, HD_BF16 = 1 } hd_dtype;
+/*
+ * HD_I8: the int8 model variant (the quantised models of Sec. II-C, which the
+ * paper mentions and does not use): X, B and C hold int8 values; Stage I sums
+ * exactly in int32 on the int8 matrix instructions, HardSign is taken on the
+ * exact sum, and Stage II is exact in fp32 (C widened to bf16, exact for
+ * int8). Every result is therefore exact: scores are integers, and labels and
+ * scores equal the mathematical definition bit for bit. Scales of a
+ * quantised model do not enter: a positive scale of X or B leaves every
+ * HardSign unchanged, and a per-class scale of C is the caller's to apply to
+ * the returned scores. Supported by hd_pack_model, hd_infer, hd_infer_packed,
+ * hd_infer_packed_noalloc, hd_bundle_classes_packed and the size and kernel
+ * queries, with HD_ACT_HARDSIGN, K <= 128, F <= 131071 (|sum| < 2^31) and
+ * D <= 131072 (|score| <= 2^24); every batch size runs on the large-batch
+ * kernels. Elsewhere HD_ERR_UNSUPPORTED.
+ */
+typedef enum { HD_F32 = 0, HD_BF16 = 1, HD_I8 = 2 } hd_dtype;
 
 /* HD_ACT_HARDSIGN is the paper's encoding activation (Sec. II-B, Eq. 3).
  * HD_ACT_IDENTITY skips it (H = X B): a linear test mode, S = X B C^T. */

@@ -19,7 +19,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libhd.so")
 
 HD_OK, HD_ERR_ARG, HD_ERR_UNSUPPORTED, HD_ERR_WORKSPACE, HD_ERR_HIP = range(5)
-HD_F32, HD_BF16 = 0, 1
+HD_F32, HD_BF16, HD_I8 = 0, 1, 2
 ACTS = {"hardsign": 0, "identity": 1}
 
 SYMBOLS = (
@@ -114,13 +114,19 @@ def _torch():
     return torch
 
 
-def _dt(t) -> int:
+def _dt_of(dtype) -> int:
     torch = _torch()
-    if t.dtype == torch.float32:
+    if dtype == torch.float32:
         return HD_F32
-    if t.dtype == torch.bfloat16:
+    if dtype == torch.bfloat16:
         return HD_BF16
-    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+    if dtype == torch.int8:
+        return HD_I8
+    raise TypeError(f"unsupported dtype {dtype}; use float32, bfloat16 or int8")
+
+
+def _dt(t) -> int:
+    return _dt_of(t.dtype)
 
 
 def _check_dev(*ts):
@@ -196,15 +202,13 @@ def similarity(H, C, return_scores: bool = False):
 
 
 def infer_workspace_bytes(N: int, F: int, D: int, K: int, dtype) -> int:
-    torch = _torch()
-    dt = HD_F32 if dtype == torch.float32 else HD_BF16
+    dt = _dt_of(dtype)
     return int(lib().hd_infer_workspace_bytes(N, F, D, K, dt))
 
 
 def infer_kernel(N: int, F: int, D: int, K: int, dtype, packed: bool = True) -> str:
     """Name of the main kernel hd_infer / hd_infer_packed launches for these sizes."""
-    torch = _torch()
-    dt = HD_F32 if dtype == torch.float32 else HD_BF16
+    dt = _dt_of(dtype)
     return lib().hd_infer_kernel(N, F, D, K, dt, 1 if packed else 0).decode()
 
 
@@ -329,8 +333,7 @@ def infer_packed_noalloc(X, model: PackedModel, act: str = "hardsign", return_sc
 
 
 def stream_workspace_bytes(nbatch: int, N: int, F: int, D: int, K: int, dtype) -> int:
-    torch = _torch()
-    dt = HD_F32 if dtype == torch.float32 else HD_BF16
+    dt = _dt_of(dtype)
     return int(lib().hd_infer_stream_workspace_bytes(nbatch, N, F, D, K, dt))
 
 
@@ -431,8 +434,7 @@ def bundle_classes_packed(X, model: PackedModel, y, K: int, counts=None):
 
 def bundle_kernel(N: int, F: int, D: int, K: int, dtype, packed: bool = True) -> str:
     """Name of the kernel bundle_classes(_packed) launches for these sizes."""
-    torch = _torch()
-    dt = HD_F32 if dtype == torch.float32 else HD_BF16
+    dt = _dt_of(dtype)
     return lib().hd_bundle_kernel(N, F, D, K, dt, 1 if packed else 0).decode()
 
 

@@ -13,7 +13,13 @@ bool dims_ok(int64_t N, int64_t F, int64_t D, int64_t K) {
   return N <= kMaxDim && F <= kMaxDim && D <= kMaxDim && K <= kMaxDim;
 }
 
-bool enums_ok(int dt, int act) { return (dt == HD_F32 || dt == HD_BF16) && (act == 0 || act == 1); }
+bool enums_ok(int dt, int act) {
+  return (dt == HD_F32 || dt == HD_BF16 || dt == HD_I8) && (act == 0 || act == 1);
+}
+
+// The int8 model variant runs on the large-batch matrix-core kernels only,
+// with the HardSign activation.
+bool i8_ok(int dt, int act) { return dt != HD_I8 || act == 0; }
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
@@ -32,6 +38,7 @@ constexpr int64_t kSmallMaxNBf16 = 8;
 constexpr int64_t kChunkedMaxN = 256;
 
 Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
+  if (dt == HD_I8) return hd::large_supported(N, F, D, K, dt) ? Route::kLarge : Route::kNone;
   const bool small_ok = N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt);
   if (small_ok && (dt == HD_F32 || N <= kSmallMaxNBf16)) return Route::kSmall;
   if (dt == HD_F32 && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
@@ -46,7 +53,7 @@ int64_t small_n(Route r, int64_t N) { return r == Route::kSmallChunked ? hd::kSm
 
 hd_status from_hip(hipError_t e) { return e == hipSuccess ? HD_OK : HD_ERR_HIP; }
 
-size_t esize(int dt) { return dt == HD_F32 ? 4 : 2; }
+size_t esize(int dt) { return dt == HD_F32 ? 4 : dt == HD_I8 ? 1 : 2; }
 
 // Packed model image: [fragment-tiled B and C for the matrix-core path |
 // column-tiled B and C for the small-batch path]. Both sections start on a
@@ -58,7 +65,7 @@ struct Image {
 Image image_layout(int64_t F, int64_t D, int64_t K, int dt) {
   Image im;
   im.large = align256(hd::large_packed_bytes(F, D, K, dt));
-  im.small = align256(hd::small_packed_bytes(F, D, K, dt));
+  im.small = dt == HD_I8 ? 0 : align256(hd::small_packed_bytes(F, D, K, dt));
   im.total = im.large + im.small;
   return im;
 }
@@ -111,7 +118,7 @@ const char* hd_status_str(hd_status s) {
 hd_status hd_encode(const void* X, const void* B, float* H, int64_t N, int64_t F, int64_t D,
                     hd_dtype dt, hd_act act, hipStream_t stream) {
   if (N < 0 || F < 1 || D < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
-  if (!dims_ok(N, F, D, 1)) return HD_ERR_UNSUPPORTED;
+  if (!dims_ok(N, F, D, 1) || dt == HD_I8) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!X || !B || !H) return HD_ERR_ARG;
   if (!aligned(X, esize(dt)) || !aligned(B, esize(dt)) || !aligned(H, 4)) return HD_ERR_ARG;
@@ -121,7 +128,7 @@ hd_status hd_encode(const void* X, const void* B, float* H, int64_t N, int64_t F
 hd_status hd_similarity(const float* H, const void* C, int32_t* labels, float* scores, int64_t N,
                         int64_t D, int64_t K, hd_dtype c_dt, hipStream_t stream) {
   if (N < 0 || D < 1 || K < 1 || !enums_ok(c_dt, 0)) return HD_ERR_ARG;
-  if (!dims_ok(N, 1, D, K)) return HD_ERR_UNSUPPORTED;
+  if (!dims_ok(N, 1, D, K) || c_dt == HD_I8) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!H || !C || !labels) return HD_ERR_ARG;
   if (!aligned(H, 4) || !aligned(C, esize(c_dt)) || !aligned(labels, 4) || !aligned(scores, 4))
@@ -161,7 +168,7 @@ hd_status hd_pack_model(const void* B, const void* C, int64_t F, int64_t D, int6
   if (packed_bytes < im.total) return HD_ERR_WORKSPACE;
   char* p = static_cast<char*>(packed);
   if (hd::launch_pack(B, C, F, D, K, dt, p, stream) != hipSuccess) return HD_ERR_HIP;
-  if (hd::launch_pack_small(B, C, F, D, K, dt, p + im.large, stream) != hipSuccess)
+  if (im.small > 0 && hd::launch_pack_small(B, C, F, D, K, dt, p + im.large, stream) != hipSuccess)
     return HD_ERR_HIP;
   return HD_OK;
 }
@@ -173,7 +180,7 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
                               int64_t K, hd_dtype dt, hd_act act, void* workspace,
                               size_t workspace_bytes, hipStream_t stream, bool dry = false) {
   if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
-  if (!dims_ok(N, F, D, K)) return HD_ERR_UNSUPPORTED;
+  if (!dims_ok(N, F, D, K) || !i8_ok(dt, act)) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!X || !labels || (packed ? false : (!B || !C))) return HD_ERR_ARG;
   const size_t es = esize(dt);
@@ -254,7 +261,7 @@ size_t hd_infer_stream_workspace_bytes(int64_t nbatch, int64_t N, int64_t F, int
   if (nbatch < 1 || N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) ||
       !dims_ok(N, F, D, K) || nbatch > kMaxDim)
     return 0;
-  if (!hd::stream_supported(N, F, D, K, dt)) return 0;
+  if (dt == HD_I8 || !hd::stream_supported(N, F, D, K, dt)) return 0;
   return hd::stream_ws_bytes(nbatch, N, K);
 }
 
@@ -270,7 +277,7 @@ hd_status hd_infer_stream(const void* X, const void* packed, const uint32_t* rea
   if (!aligned(X, 4) || !aligned(packed, 256) || !aligned(labels, 4) || !aligned(scores, 4) ||
       !aligned(ready, 4) || !aligned(done, 4) || !aligned(workspace, 256))
     return HD_ERR_ARG;
-  if (!hd::stream_supported(N, F, D, K, dt)) return HD_ERR_UNSUPPORTED;
+  if (dt == HD_I8 || !hd::stream_supported(N, F, D, K, dt)) return HD_ERR_UNSUPPORTED;
   if (workspace_bytes < hd::stream_ws_bytes(nbatch, N, K)) return HD_ERR_WORKSPACE;
   const char* small = static_cast<const char*>(packed) + image_layout(F, D, K, dt).large;
   return from_hip(hd::launch_stream(X, small, ready, labels, scores, done, nbatch, N, F, D, K,
@@ -281,7 +288,7 @@ hd_status hd_bundle_classes(const void* X, const void* B, const int32_t* y, int3
                             int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt,
                             hipStream_t stream) {
   if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0)) return HD_ERR_ARG;
-  if (!dims_ok(N, F, D, K) || !hd::bundle_supported(K)) return HD_ERR_UNSUPPORTED;
+  if (!dims_ok(N, F, D, K) || !hd::bundle_supported(K) || dt == HD_I8) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!X || !B || !y || !counts) return HD_ERR_ARG;
   if (!aligned(X, esize(dt)) || !aligned(B, esize(dt)) || !aligned(y, 4) || !aligned(counts, 4))
@@ -305,7 +312,7 @@ hd_status hd_bundle_classes_packed(const void* X, const void* packed, const int3
 const char* hd_bundle_kernel(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, int packed) {
   if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return "";
   if (packed) return hd::bundle_packed_kernel_name(N, F, D, K, dt);
-  return hd::bundle_supported(K) ? "bundle_valu_kernel" : "";
+  return hd::bundle_supported(K) && dt != HD_I8 ? "bundle_valu_kernel" : "";
 }
 
 hd_status hd_class_hardsign(const int32_t* counts, float* M, int64_t K, int64_t D,

@@ -61,6 +61,16 @@ struct TrBF16 {
   static constexpr int kFStep = 16;
   static constexpr int kVec = 8;  // elements per 16-byte group
   static constexpr int kEsz = 2;
+  // element e of a 16-byte group held as four dwords: set, read, clear
+  __device__ static void put(uint32_t (&t)[4], int e, elem x) {
+    t[e >> 1] |= (uint32_t)x << (16 * (e & 1));
+  }
+  __device__ static elem get(const uint32_t (&t)[4], int e) {
+    return (uint16_t)(t[e >> 1] >> (16 * (e & 1)));
+  }
+  __device__ static void clear(uint32_t (&t)[4], int e) { t[e >> 1] &= ~(0xffffu << (16 * (e & 1))); }
+  // Stage I accumulator value v is >= 0 (the HardSign test, Eq. 1)
+  __device__ static bool nonneg(float v) { return v >= 0.0f; }
   static constexpr int kStage1Mfma = 1;  // matrix instructions per stage1 call
   static constexpr int kCFrags = 2;  // 1 KiB C fragments per (d-block, class block)
   // LDS position of feature column c inside a sample row.
@@ -81,6 +91,10 @@ struct TrF32 {
   static constexpr int kFStep = 8;
   static constexpr int kVec = 4;
   static constexpr int kEsz = 4;
+  __device__ static void put(uint32_t (&t)[4], int e, elem x) { t[e] = __float_as_uint(x); }
+  __device__ static elem get(const uint32_t (&t)[4], int e) { return __uint_as_float(t[e]); }
+  __device__ static void clear(uint32_t (&t)[4], int e) { t[e] = 0u; }
+  __device__ static bool nonneg(float v) { return v >= 0.0f; }
   static constexpr int kStage1Mfma = 4;
   static constexpr int kCFrags = 4;
   // Within each group of 8 features the even ones are stored first, so a
@@ -106,6 +120,48 @@ struct TrF32 {
   }
 };
 
+// int8 model variant: X and B int8, Stage I on the int8 matrix instruction
+// with exact int32 accumulation (the accumulator registers hold the int32
+// bits), HardSign on the exact integer; Stage II takes C widened to bf16
+// (exact for |c| <= 128) through the bf16 path. One f-step is 32 features.
+struct TrI8 {
+  typedef int8_t elem;
+  static constexpr int kFStep = 32;
+  static constexpr int kVec = 16;
+  static constexpr int kEsz = 1;
+  static constexpr int kStage1Mfma = 1;
+  static constexpr int kCFrags = 2;  // C tiles are the bf16 ones
+  __device__ static void put(uint32_t (&t)[4], int e, elem x) {
+    t[e >> 2] |= (uint32_t)(uint8_t)x << (8 * (e & 3));
+  }
+  __device__ static elem get(const uint32_t (&t)[4], int e) {
+    return (int8_t)(uint8_t)(t[e >> 2] >> (8 * (e & 3)));
+  }
+  __device__ static void clear(uint32_t (&t)[4], int e) { t[e >> 2] &= ~(0xffu << (8 * (e & 3))); }
+  __device__ static bool nonneg(float v) { return __float_as_int(v) >= 0; }
+  __device__ static int lds_pos(int c) { return c; }
+  __device__ static void stage1(f32x16& acc, const uint4& a, const uint4& b) {
+    acc = bitcast<f32x16>(__builtin_amdgcn_mfma_i32_32x32x32_i8(
+        bitcast<i32x4>(a), bitcast<i32x4>(b), bitcast<i32x16>(acc), 0, 0, 0));
+  }
+  __device__ static void stage1_init(f32x16& acc, const uint4& a, const uint4& b) {
+    acc = bitcast<f32x16>(
+        __builtin_amdgcn_mfma_i32_32x32x32_i8(bitcast<i32x4>(a), bitcast<i32x4>(b), i32x16{}, 0, 0, 0));
+  }
+};
+
+// Largest sizes of the int8 variant for which every sum is exact: |V| <=
+// 128 * 128 * F < 2^31 in int32, and |S| <= 128 * D <= 2^24 in fp32.
+constexpr int64_t kI8MaxF = (int64_t(1) << 17) - 1;
+constexpr int64_t kI8MaxD = int64_t(1) << 17;
+
+// LDS row padding of an X tile: one 16-byte group (keeps the 32 rows read by
+// one fragment load on distinct LDS banks).
+template <class Tr>
+constexpr int pad_of() {
+  return 16 / Tr::kEsz;
+}
+
 // Number of f-steps and padded row pitch (elements) of the LDS X tile.
 template <class Tr>
 __host__ __device__ inline int nfs_of(int F) {
@@ -115,7 +171,7 @@ template <class Tr>
 __host__ __device__ inline int pitch_of(int F) {
   // Padding by half a 16-byte group (bf16) / one group (fp32) keeps the
   // 32 rows read by one fragment load on distinct LDS banks.
-  return nfs_of<Tr>(F) * Tr::kFStep + (Tr::kEsz == 2 ? 8 : 4);
+  return nfs_of<Tr>(F) * Tr::kFStep + pad_of<Tr>();
 }
 
 // ---------------------------------------------------------------------------
@@ -143,7 +199,7 @@ inline int kb_of(int64_t K) {
 // fit in registers, fewer as class blocks grow.
 template <class Tr>
 constexpr int chunk_ntiles(int kb) {
-  return kb > 2 ? (Tr::kEsz == 2 ? 2 : 1) : kb == 2 ? 2 : 4;
+  return kb > 2 ? (Tr::kEsz <= 2 ? 2 : 1) : kb == 2 ? 2 : 4;
 }
 
 template <class Tr>
@@ -189,6 +245,43 @@ __global__ void pack_b_f32(const float* __restrict__ B, uint4* __restrict__ Bp, 
   }
   Bp[frag * 64 + l] = make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
                                  __float_as_uint(v[2]), __float_as_uint(v[3]));
+}
+
+__global__ void pack_b_i8(const int8_t* __restrict__ B, uint4* __restrict__ Bp, int F, int D,
+                          int ndb, int nfs) {
+  const int64_t frag = blockIdx.x;
+  const int l = threadIdx.x;
+  if (frag >= (int64_t)ndb * nfs) return;
+  const int db = (int)(frag / nfs), fs = (int)(frag % nfs);
+  const int d = 32 * db + (l & 31);
+  uint32_t t[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int f = 32 * fs + 16 * (l >> 5) + e;
+    if (f < F && d < D) TrI8::put(t, e, B[(int64_t)f * D + d]);
+  }
+  Bp[frag * 64 + l] = make_uint4(t[0], t[1], t[2], t[3]);
+}
+
+// int8 C into the bf16 C tiles (an int8 value is exact in bf16).
+__global__ void pack_c_i8(const int8_t* __restrict__ C, uint4* __restrict__ Cp, int D, int K,
+                          int ndb, int kb) {
+  const int64_t frag = blockIdx.x;
+  const int l = threadIdx.x;
+  if (frag >= (int64_t)ndb * 2 * kb) return;
+  const int kbi = (int)(frag % kb);
+  const int h = (int)((frag / kb) % 2);
+  const int db = (int)(frag / (2 * kb));
+  const int k = 32 * kbi + (l & 31);
+  uint32_t v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int d = 32 * db + 16 * h + 4 * (l >> 5) + (e < 4 ? e : 8 + e - 4);
+    const float c = (k < K && d < D) ? (float)C[(int64_t)k * D + d] : 0.0f;
+    v[e] = __float_as_uint(c) >> 16;
+  }
+  Cp[frag * 64 + l] = make_uint4(v[0] | v[1] << 16, v[2] | v[3] << 16, v[4] | v[5] << 16,
+                                 v[6] | v[7] << 16);
 }
 
 // grid: ndb * 2 * kb fragments of 64 lanes.
@@ -346,6 +439,17 @@ struct CFrags<TrF32, KB> {
   template <int ACT>
   __device__ void apply(const f32x16& v, int b, f32x16 (&s)[KB]) const {
     stage2_f32<KB, ACT>(v, f[b], s);
+  }
+};
+
+template <int KB>
+struct CFrags<TrI8, KB> : CFrags<TrBF16, KB> {
+  template <int ACT>
+  __device__ void apply(const f32x16& v, int b, f32x16 (&s)[KB]) const {
+    f32x16 vf;  // the exact int32 sums as floats (sign and zero preserved)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) vf[r] = (float)__float_as_int(v[r]);
+    stage2_bf16<KB, ACT>(vf, this->f[b], s);
   }
 };
 
@@ -519,10 +623,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
         const int64_t first = (g0 + g) * Tr::kVec;
         for (int j = 0; j < Tr::kVec; ++j) {
           if (first + j >= nx_total) break;
-          if constexpr (Tr::kEsz == 2)
-            t[j >> 1] |= (uint32_t)X[first + j] << (16 * (j & 1));
-          else
-            t[j] = __float_as_uint(X[first + j]);
+          Tr::put(t, j, X[first + j]);
         }
         w = make_uint4(t[0], t[1], t[2], t[3]);
       }
@@ -532,15 +633,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
       const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
       for (int j = 0; j < Tr::kVec; ++j) {
-        if (e >= 0 && r < rows) {
-          T val;
-          if constexpr (Tr::kEsz == 2) {
-            val = (uint16_t)(ws[j >> 1] >> (16 * (j & 1)));
-          } else {
-            val = __uint_as_float(ws[j]);
-          }
-          xt[r * pitch + Tr::lds_pos(c)] = val;
-        }
+        if (e >= 0 && r < rows) xt[r * pitch + Tr::lds_pos(c)] = Tr::get(ws, j);
         ++e;
         if (e == 0) {
           r = 0;
@@ -702,7 +795,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nfs = nfs_of<Tr>(F);
   const int nchunks = (nfs + fsc - 1) / fsc;
-  const int pitch = fsc * Tr::kFStep + (Tr::kEsz == 2 ? 8 : 4);  // elements
+  const int pitch = fsc * Tr::kFStep + pad_of<Tr>();  // elements
   const int ntiles = (int)cdiv(N, NT);
   const int slice = blockIdx.x % DS;
   const int tile = blockIdx.x / DS;
@@ -743,11 +836,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_kernel(
 #pragma unroll
             for (int e = 0; e < Tr::kVec; ++e) {
               const int ce = c + e < F ? c + e : F - 1;
-              const T x = xr[ce];
-              if constexpr (Tr::kEsz == 2)
-                t[e >> 1] |= (uint32_t)x << (16 * (e & 1));
-              else
-                t[e] = __float_as_uint(x);
+              Tr::put(t, e, xr[ce]);
             }
             w[j][g] = make_uint4(t[0], t[1], t[2], t[3]);
           }
@@ -767,20 +856,15 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_kernel(
             uint32_t t[4] = {w[j][g].x, w[j][g].y, w[j][g].z, w[j][g].w};
 #pragma unroll
             for (int e = 0; e < Tr::kVec; ++e)
-              if (c + e >= F) {
-                if constexpr (Tr::kEsz == 2)
-                  t[e >> 1] &= ~(0xffffu << (16 * (e & 1)));
-                else
-                  t[e] = 0u;
-              }
+              if (c + e >= F) Tr::clear(t, e);
             w[j][g] = make_uint4(t[0], t[1], t[2], t[3]);
           }
         }
         uint4* dst = reinterpret_cast<uint4*>(xt + r * pitch + s * Tr::kFStep);
-        if constexpr (Tr::kEsz == 2) {
+        if constexpr (Tr::kEsz != 4) {
           dst[0] = w[j][0];
           dst[1] = w[j][1];
-        } else {
+        } else {  // fp32: even features of the step first (lds_pos)
           dst[0] = make_uint4(w[j][0].x, w[j][0].z, w[j][1].x, w[j][1].z);
           dst[1] = make_uint4(w[j][0].y, w[j][0].w, w[j][1].y, w[j][1].w);
         }
@@ -1169,11 +1253,7 @@ __device__ __forceinline__ void bundle_stage(typename Tr::elem* xt, const typena
 #pragma unroll
           for (int e = 0; e < Tr::kVec; ++e) {
             const int ce = c + e < F ? c + e : F - 1;
-            const T x = xr[ce];
-            if constexpr (Tr::kEsz == 2)
-              t[e >> 1] |= (uint32_t)x << (16 * (e & 1));
-            else
-              t[e] = __float_as_uint(x);
+            Tr::put(t, e, xr[ce]);
           }
           w[j][g] = make_uint4(t[0], t[1], t[2], t[3]);
         }
@@ -1194,20 +1274,15 @@ __device__ __forceinline__ void bundle_stage(typename Tr::elem* xt, const typena
           uint32_t t[4] = {w[j][g].x, w[j][g].y, w[j][g].z, w[j][g].w};
 #pragma unroll
           for (int e = 0; e < Tr::kVec; ++e)
-            if (c + e >= F) {
-              if constexpr (Tr::kEsz == 2)
-                t[e >> 1] &= ~(0xffffu << (16 * (e & 1)));
-              else
-                t[e] = 0u;
-            }
+            if (c + e >= F) Tr::clear(t, e);
           w[j][g] = make_uint4(t[0], t[1], t[2], t[3]);
         }
       }
       uint4* dst = reinterpret_cast<uint4*>(xt + r * pitch + s * Tr::kFStep);
-      if constexpr (Tr::kEsz == 2) {
+      if constexpr (Tr::kEsz != 4) {
         dst[0] = w[j][0];
         dst[1] = w[j][1];
-      } else {
+      } else {  // fp32: even features of the step first (lds_pos)
         dst[0] = make_uint4(w[j][0].x, w[j][0].z, w[j][1].x, w[j][1].z);
         dst[1] = make_uint4(w[j][0].y, w[j][0].w, w[j][1].y, w[j][1].w);
       }
@@ -1228,7 +1303,7 @@ __global__ __launch_bounds__(kThreads, OCC) void bundle_mfma_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nfs = nfs_of<Tr>(F);
   const int nchunks = (nfs + fsc - 1) / fsc;
-  const int pitch = fsc * Tr::kFStep + (Tr::kEsz == 2 ? 8 : 4);  // elements
+  const int pitch = fsc * Tr::kFStep + pad_of<Tr>();  // elements
   const int units = ndb / 2;
   const int ncg = (units + kWaves - 1) / kWaves;
   const int cg = blockIdx.x % ncg;
@@ -1331,7 +1406,7 @@ __global__ __launch_bounds__(kThreads, OCC) void bundle_mfma_kernel(
 #pragma unroll
             for (int b = 0; b < 2; ++b)
               atomicAdd(&cnt[k * kBundleCols + wave * 64 + 32 * b + xrow],
-                        vacc[b][t][r] >= 0.0f ? 1 : -1);
+                        Tr::nonneg(vacc[b][t][r]) ? 1 : -1);
           }
         }
     }
@@ -1541,7 +1616,7 @@ __global__ __launch_bounds__(kThreads, 1) void bundle_dma_kernel(
 #pragma unroll
             for (int b = 0; b < 2; ++b)
               atomicAdd(&cnt[k * kCols + (j * kWaves + wave) * 64 + 32 * b + xrow],
-                        vacc[j][b][t][r] >= 0.0f ? 1 : -1);
+                        Tr::nonneg(vacc[j][b][t][r]) ? 1 : -1);
           }
         }
     }
@@ -1570,10 +1645,19 @@ struct LargeCfg {
   bool ok;
 };
 
+// Calls f with the element traits of dt (0 fp32, 1 bf16, 2 int8).
+template <class Fn>
+auto with_traits(int dt, Fn&& f) {
+  if (dt == 0) return f(TrF32{});
+  if (dt == 2) return f(TrI8{});
+  return f(TrBF16{});
+}
+
 template <class Tr>
 LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) {
   LargeCfg c{};
   if (cdiv(K, 32) > 4 || F > (1 << 20) || N > (1 << 30)) return c;
+  if (Tr::kEsz == 1 && (F > kI8MaxF || D > kI8MaxD)) return c;
   // B fragments are addressed with 32-bit byte offsets
   if (cdiv(D, 64) * 2 * nfs_of<Tr>((int)F) * 1024 >= ((int64_t)1 << 31)) return c;
   const int pitch = pitch_of<Tr>((int)F);
@@ -1593,7 +1677,7 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) 
     // X tile too large for LDS: stream it in chunks of f-steps
     const int nt = chunk_ntiles<Tr>(kbr);
     const size_t rbytes = (size_t)kWaves * 32 * nt * 32 * kbr * 4;
-    const int pad = Tr::kEsz == 2 ? 8 : 4;
+    const int pad = pad_of<Tr>();
     const int64_t cols = ((int64_t)kLdsBytes - 16) / (32 * nt * Tr::kEsz) - pad;
     const int fsc = (int)(cols / Tr::kFStep);
     if (fsc < 8 || rbytes > (size_t)kLdsBytes) return c;
@@ -1722,6 +1806,7 @@ template <class Tr>
 BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) {
   BundleCfg c{};
   if (K < 1 || K > kBundleMfmaMaxK || F > (1 << 20) || N > (1 << 30) || N < 1) return c;
+  if (Tr::kEsz == 1 && F > kI8MaxF) return c;
   if (cdiv(D, 64) * 2 * nfs_of<Tr>((int)F) * 1024 >= ((int64_t)1 << 31)) return c;
   if (Tr::kEsz == 2 && F % 8 == 0 && x16) {
     // double-buffered kernel: two units per wave while the class counters fit
@@ -1746,10 +1831,10 @@ BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true
       }
     }
   }
-  c.nt = Tr::kEsz == 2 ? 4 : 2;
-  c.occ = Tr::kEsz == 2 ? 1 : 2;
+  c.nt = Tr::kEsz <= 2 ? 4 : 2;
+  c.occ = Tr::kEsz <= 2 ? 1 : 2;
   const int nfs = nfs_of<Tr>((int)F);
-  const int pad = Tr::kEsz == 2 ? 8 : 4;
+  const int pad = pad_of<Tr>();
   const size_t fixed = 16 + sizeof(int) * (32 * c.nt + (size_t)K * kBundleCols);
   const size_t per_row = (size_t)32 * c.nt * Tr::kEsz;  // bytes per LDS column of the tile
   // Two workgroups per compute unit (fp32) while the class counters leave
@@ -1775,11 +1860,12 @@ BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true
 }  // namespace
 
 bool bundle_packed_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  return dt == 0 ? bundle_cfg<TrF32>(N, F, D, K).ok : bundle_cfg<TrBF16>(N, F, D, K).ok;
+  return with_traits(dt, [&](auto tr) { return bundle_cfg<decltype(tr)>(N, F, D, K).ok; });
 }
 
 const char* bundle_packed_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   if (dt == 0) return bundle_cfg<TrF32>(N, F, D, K).ok ? "bundle_mfma_kernel" : "";
+  if (dt == 2) return bundle_cfg<TrI8>(N, F, D, K).ok ? "bundle_mfma_kernel" : "";
   const BundleCfg c = bundle_cfg<TrBF16>(N, F, D, K);
   if (!c.ok) return "";
   return c.dma_upw > 0 ? "bundle_dma_kernel" : "bundle_mfma_kernel";
@@ -1799,6 +1885,16 @@ hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t
     hipLaunchKernelGGL(k, dim3((unsigned)(c.ncg * c.ngroups)), block, c.lds, stream,
                        (const float*)X, (const uint4*)packed, y, counts, (int)N, (int)F, (int)D,
                        (int)K, g.ndb, c.ngroups, c.fsc);
+  } else if (dt == 2) {
+    const BundleCfg c = bundle_cfg<TrI8>(N, F, D, K);
+    if (!c.ok) return hipErrorInvalidValue;
+    const PackGeom g = pack_geom<TrI8>(F, D, 1);
+    auto* k = &bundle_mfma_kernel<TrI8, 4, 1>;
+    const hipError_t a = allow_large_lds<&bundle_mfma_kernel<TrI8, 4, 1>>();
+    if (a != hipSuccess) return a;
+    hipLaunchKernelGGL(k, dim3((unsigned)(c.ncg * c.ngroups)), block, c.lds, stream,
+                       (const int8_t*)X, (const uint4*)packed, y, counts, (int)N, (int)F,
+                       (int)D, (int)K, g.ndb, c.ngroups, c.fsc);
   } else {
     const BundleCfg c = bundle_cfg<TrBF16>(N, F, D, K, ((uintptr_t)X % 16) == 0);
     if (!c.ok) return hipErrorInvalidValue;
@@ -1831,25 +1927,26 @@ hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t
 }
 
 bool large_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  return dt == 0 ? large_cfg<TrF32>(N, F, D, K).ok : large_cfg<TrBF16>(N, F, D, K).ok;
+  return with_traits(dt, [&](auto tr) { return large_cfg<decltype(tr)>(N, F, D, K).ok; });
 }
 
 const char* large_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  const LargeCfg c = dt == 0 ? large_cfg<TrF32>(N, F, D, K) : large_cfg<TrBF16>(N, F, D, K);
+  const LargeCfg c =
+      with_traits(dt, [&](auto tr) { return large_cfg<decltype(tr)>(N, F, D, K); });
   if (!c.ok) return "";
   if (c.fsc > 0) return c.dma ? "large_chunked_dma_kernel" : "large_chunked_kernel";
   return "large_fused_kernel";
 }
 
 size_t large_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {
-  const PackGeom g = dt == 0 ? pack_geom<TrF32>(F, D, K) : pack_geom<TrBF16>(F, D, K);
+  const PackGeom g = with_traits(dt, [&](auto tr) { return pack_geom<decltype(tr)>(F, D, K); });
   return g.b_bytes + g.c_bytes;
 }
 
 size_t large_workspace_bytes_for(int64_t N, int64_t F, int64_t D, int64_t K, int dt,
                                  bool x16) {
   const LargeCfg c =
-      dt == 0 ? large_cfg<TrF32>(N, F, D, K, x16) : large_cfg<TrBF16>(N, F, D, K, x16);
+      with_traits(dt, [&](auto tr) { return large_cfg<decltype(tr)>(N, F, D, K, x16); });
   if (!c.ok || c.ds == 1) return 0;
   const size_t cbytes = ((size_t)c.ntiles * sizeof(unsigned) + 255) / 256 * 256;
   return cbytes + sizeof(float) * (size_t)c.ds * N * K;
@@ -1873,6 +1970,14 @@ hipError_t launch_pack(const void* B, const void* C, int64_t F, int64_t D, int64
                        (const float*)B, Bp, (int)F, (int)D, g.ndb, g.nfs);
     hipLaunchKernelGGL(pack_c_f32, dim3((unsigned)((int64_t)g.ndb * g.kb * 4)), dim3(64), 0,
                        stream, (const float*)C, Cp, (int)D, C ? (int)K : 0, g.ndb, g.kb);
+  } else if (dt == 2) {
+    const PackGeom g = pack_geom<TrI8>(F, D, K);
+    uint4* Bp = (uint4*)packed;
+    uint4* Cp = (uint4*)((char*)packed + g.b_bytes);
+    hipLaunchKernelGGL(pack_b_i8, dim3((unsigned)((int64_t)g.ndb * g.nfs)), dim3(64), 0, stream,
+                       (const int8_t*)B, Bp, (int)F, (int)D, g.ndb, g.nfs);
+    hipLaunchKernelGGL(pack_c_i8, dim3((unsigned)((int64_t)g.ndb * 2 * g.kb)), dim3(64), 0,
+                       stream, (const int8_t*)C, Cp, (int)D, C ? (int)K : 0, g.ndb, g.kb);
   } else {
     const PackGeom g = pack_geom<TrBF16>(F, D, K);
     uint4* Bp = (uint4*)packed;
@@ -1890,6 +1995,8 @@ hipError_t launch_large(const void* X, const void* packed, int32_t* labels, floa
                         void* workspace, hipStream_t stream) {
   if (dt == 0)
     return launch_tr<TrF32>(X, packed, labels, scores, N, F, D, K, act, workspace, stream);
+  if (dt == 2)
+    return launch_tr<TrI8>(X, packed, labels, scores, N, F, D, K, act, workspace, stream);
   return launch_tr<TrBF16>(X, packed, labels, scores, N, F, D, K, act, workspace, stream);
 }
 

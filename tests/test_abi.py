@@ -182,3 +182,24 @@ def test_packed_training_argument_errors(L):
     assert f(FAKE, FAKE, FAKE, FAKE, 4, 8, 64, 3, 5, None) == hd.HD_ERR_ARG
     # a model packed without a codebook: C may be NULL, B may not
     assert L.hd_pack_model(None, None, 8, 16, 3, 0, FAKE, 1 << 30, None) == hd.HD_ERR_ARG
+
+
+def test_int8_limits(L):
+    """The int8 variant: HardSign only, exactness bounds on F and D, the
+    large-batch kernels for every batch size, no stage-alone or streaming call."""
+    I8 = hd.HD_I8
+    assert _infer(L, dt=I8, act=1) == hd.HD_ERR_UNSUPPORTED
+    assert _infer(L, dt=I8, F=131072) == hd.HD_ERR_UNSUPPORTED
+    assert _infer(L, dt=I8, D=131073) == hd.HD_ERR_UNSUPPORTED
+    assert _infer(L, dt=I8, K=129) == hd.HD_ERR_UNSUPPORTED
+    assert L.hd_infer_kernel(1, 561, 10240, 6, I8, 1) == b"large_fused_kernel"
+    assert L.hd_infer_kernel(1, 131071, 64, 2, I8, 1) == b"large_chunked_kernel"
+    assert L.hd_encode(FAKE, FAKE, FAKE, 4, 8, 16, I8, 0, None) == hd.HD_ERR_UNSUPPORTED
+    assert L.hd_similarity(FAKE, FAKE, FAKE, None, 4, 16, 3, I8, None) == hd.HD_ERR_UNSUPPORTED
+    assert L.hd_bundle_classes(FAKE, FAKE, FAKE, FAKE, 4, 8, 64, 3, I8, None) == \
+        hd.HD_ERR_UNSUPPORTED
+    assert L.hd_infer_stream_workspace_bytes(4, 1, 561, 10240, 6, I8) == 0
+    assert L.hd_bundle_kernel(100, 617, 4096, 26, I8, 1) == b"bundle_mfma_kernel"
+    assert L.hd_bundle_kernel(100, 617, 4096, 26, I8, 0) == b""
+    # the packed image has no small-batch section
+    assert L.hd_model_packed_bytes(617, 4096, 26, I8) < L.hd_model_packed_bytes(617, 4096, 26, 1)
