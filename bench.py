@@ -10,6 +10,8 @@ and the CPU oracle's throughput on a bounded sample as a baseline.
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
     python bench.py --sweep-d     # N = 1, F = 3072, K = 10: one line per D (bandwidth map)
     python bench.py --sweep-n     # F = 561, D = 10240, K = 6: one line per N (samples/s curve)
+    python bench.py --workload speech --dtype i8      # the int8 model variant
+    python bench.py --workload colour_k10 --train     # single-pass training (Sec. II-C)
 """
 from __future__ import annotations
 
@@ -32,7 +34,10 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 METRIC = "inference samples/sec at D=10240 (N=1..65536); % HBM / MFMA roofline"
 HBM_PEAK_GBS = 8000.0
-MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3, "i8": 5000.0}  # dense; i8 in TOP/s
+PEAK_UNIT = {"bf16": "TFLOP/s", "f32": "TFLOP/s", "i8": "TOP/s"}
+ESIZE = {"f32": 4, "bf16": 2, "i8": 1}
+TRAIN_METRIC = "single-pass training samples/sec (class hypervectors from N labelled samples)"
 MALL_BYTES = 256 << 20
 
 # workload -> (dtype, path description)
@@ -46,7 +51,11 @@ def parse():
     p.add_argument("--steps", type=int, default=None)
     p.add_argument("--warmup", type=int, default=None)
     p.add_argument("--workload", default="activity_n32", choices=sorted(hd_inputs.WORKLOADS))
-    p.add_argument("--dtype", default=None, choices=["f32", "bf16"])
+    p.add_argument("--dtype", default=None, choices=["f32", "bf16", "i8"])
+    p.add_argument("--train", action="store_true",
+                   help="single-pass training: one step = clear the class counts, "
+                        "hd_bundle_classes_packed over the workload's N labelled samples, "
+                        "hd_class_hardsign")
     p.add_argument("--copies", type=int, default=0,
                    help="distinct model copies rotated per step (0 = enough to exceed the MALL)")
     p.add_argument("--no-graph", action="store_true", help="time an eager loop instead of a graph")
@@ -97,7 +106,111 @@ def main():
     if args.stream:
         run_stream(args, w)
         return
+    if args.train:
+        run_train(args, w)
+        return
     run(args, w)
+
+
+def make_data(w, dtype, seed=0):
+    """The workload's X, B, C as float32 (f32, bf16-rounded for bf16) or int8."""
+    if dtype == "i8":
+        return hd_inputs.make_int8_inputs(w.N, w.F, w.D, w.K, seed=seed)
+    return hd_inputs.make_inputs(w.N, w.F, w.D, w.K, w.x_dist, seed=seed, dtype=dtype)
+
+
+def to_device(a, dtype, dev):
+    import torch
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+    if dtype == "i8":
+        return torch.from_numpy(np.ascontiguousarray(a, np.int8)).to(dev)
+    return torch.from_numpy(hd_inputs.bf16_bits(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+
+def run_train(args, w):
+    """One step = one single-pass training over the workload's N samples with
+    uniform labels: counts cleared (a fill kernel), class sums of
+    HardSign(X B) (hd_bundle_classes_packed, B tiled once before timing),
+    codebook = HardSign(counts) (hd_class_hardsign)."""
+    import torch
+    import paper_2506_09282_amd as hd
+
+    dtype = args.dtype or BENCH_DTYPE[args.workload]
+    steps = args.steps or 20
+    warmup = args.warmup if args.warmup is not None else 3
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print(f"[bench] train workload={w.name} N={w.N} F={w.F} D={w.D} K={w.K} dtype={dtype} "
+          f"steps={steps} warmup={warmup}", file=sys.stderr, flush=True)
+    X, B, _ = make_data(w, dtype)
+    y = np.random.default_rng(1).integers(0, w.K, w.N).astype(np.int32)
+    Xd, Bd = to_device(X, dtype, dev), to_device(B, dtype, dev)
+    yd = torch.from_numpy(y).to(dev)
+    model = hd.pack_model(Bd, K=w.K)
+    counts = torch.zeros((w.K, w.D), dtype=torch.int32, device=dev)
+    M = torch.empty((w.K, w.D), dtype=torch.float32, device=dev)
+    kernel = hd.bundle_kernel(w.N, w.F, w.D, w.K, Xd.dtype, packed=True)
+    stream = torch.cuda.Stream(device=dev)
+
+    def step():
+        counts.zero_()
+        hd.bundle_classes_packed(Xd, model, yd, w.K, counts=counts)
+        hd.class_hardsign(counts, out=M)
+
+    with torch.cuda.stream(stream):
+        for _ in range(warmup):
+            step()
+    stream.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        for _ in range(steps):
+            step()
+        ev1.record(stream)
+    ev1.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    value = w.N / (ms / 1e3)
+    flops = 2.0 * w.N * w.F * w.D
+    roof = {"bound": "mfma", "achieved": flops / (ms / 1e3) / 1e12,
+            "peak": MFMA_PEAK_TFLOPS[dtype], "unit": PEAK_UNIT[dtype], "traffic": None,
+            "kernel_time": "whole step (fill + class sums + HardSign)"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()}
+    out = {
+        "metric": TRAIN_METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name} training: N={w.N} labelled samples, F={w.F} "
+                               f"D={w.D} K={w.K}, labels uniform, X~{w.x_dist if dtype != 'i8' else 'U{-128..127}'}, seed 0",
+                   "global_batch": w.N, "parallelism": "single GPU", "kernel": kernel,
+                   "model": "B tiled once before timing"},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_train(w, X, B, y, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_train(w, X, B, y, target_s):
+    """The oracle's bundle on the host cores over a bounded prefix of the
+    training set (about target_s seconds)."""
+    import oracle
+    orc = oracle.default()
+    threads = orc.threads(0)
+    n_probe = min(w.N, 8 * threads)
+    t0 = time.perf_counter()
+    orc.bundle(X[:n_probe], B, y[:n_probe], w.K)
+    per = (time.perf_counter() - t0) / n_probe
+    n = int(max(1, min(w.N, target_s / max(per, 1e-9))))
+    t0 = time.perf_counter()
+    orc.bundle(X[:n], B, y[:n], w.K)
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt, 3), "unit": "samples/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "sample": f"the first {n} of the {w.N} labelled samples, float64 loops, "
+                      f"{dt:.1f} s on {threads} threads"}
 
 
 def run_stream(args, w):
@@ -174,14 +287,12 @@ def run(args, w):
     print(f"[bench] workload={w.name} N={w.N} F={w.F} D={w.D} K={w.K} dtype={dtype} "
           f"steps={steps} warmup={warmup}", file=sys.stderr, flush=True)
 
-    X, B, C = hd_inputs.make_inputs(w.N, w.F, w.D, w.K, w.x_dist, seed=0, dtype=dtype)
+    X, B, C = make_data(w, dtype)
 
     def up(a):
-        if dtype == "f32":
-            return torch.from_numpy(a).to(dev)
-        return torch.from_numpy(hd_inputs.bf16_bits(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        return to_device(a, dtype, dev)
 
-    esz = 4 if dtype == "f32" else 2
+    esz = ESIZE[dtype]
     model_bytes = esz * (w.F * w.D + w.K * w.D)
     copies = args.copies or (max(1, -(-2 * MALL_BYTES // model_bytes)) if small else 1)
     Xd = up(X)
@@ -199,7 +310,7 @@ def run(args, w):
 
     stream = torch.cuda.Stream(device=dev)
     ws_bytes = int(hd.lib().hd_infer_packed_workspace_bytes(
-        w.N, w.F, w.D, w.K, hd.HD_F32 if dtype == "f32" else hd.HD_BF16))
+        w.N, w.F, w.D, w.K, {"f32": hd.HD_F32, "bf16": hd.HD_BF16, "i8": hd.HD_I8}[dtype]))
     ws = torch.zeros(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
 
     def step(i):
@@ -263,7 +374,7 @@ def run(args, w):
     else:
         flops = 2.0 * w.N * w.D * (w.F + w.K)
         roof = {"bound": "mfma", "achieved": flops / launch_s / 1e12,
-                "peak": MFMA_PEAK_TFLOPS[dtype], "unit": "TFLOP/s", "traffic": traffic}
+                "peak": MFMA_PEAK_TFLOPS[dtype], "unit": PEAK_UNIT[dtype], "traffic": traffic}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()}
 
@@ -273,7 +384,9 @@ def run(args, w):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.note}; N={w.N} F={w.F} D={w.D} K={w.K} "
-                               f"X~{w.x_dist}, B,C~N(0,1), HardSign, seed 0",
+                               + (f"X~{w.x_dist}, B,C~N(0,1)" if dtype != "i8"
+                                  else "X,B,C~U{-128..127} (int8 model variant)")
+                               + ", HardSign, seed 0",
                    "global_batch": w.N, "parallelism": "single GPU",
                    "model_copies_rotated": copies, "timing": "hip graph" if use_graph else "eager",
                    "kernel": kernel, "model": "packed once before timing"},
@@ -299,7 +412,7 @@ def run(args, w):
 
 def alg_bytes_of(w, dtype) -> int:
     """Algorithmic bytes of one call: X, B and C read once, labels written."""
-    esz = 4 if dtype == "f32" else 2
+    esz = ESIZE[dtype]
     return esz * (w.N * w.F + w.F * w.D + w.K * w.D) + 4 * w.N
 
 
