@@ -1420,32 +1420,36 @@ __global__ __launch_bounds__(kThreads, OCC) void bundle_mfma_kernel(
   }
 }
 
-// bf16 training with the X chunks double-buffered in LDS and filled by
-// buffer-to-LDS loads, on the schedule of large_chunked_dma_kernel: 64-sample
+// bf16 and int8 training with the X chunks double-buffered in LDS and filled
+// by buffer-to-LDS loads, on the schedule of large_chunked_dma_kernel: 64-sample
 // tiles, chunks of kDmaFsc f-steps, the next chunk's loads issued two per
 // f-step at the start of the current one, the B fragment ring running on
 // across chunks and tiles (a wave keeps its units for every tile). The
 // labels of the tile a chunk belongs to travel with it: one 4-byte
 // buffer-to-LDS load per wave at the chunk's first step (every wave writes the
 // same values) into a label buffer selected by tile parity.
-// Requires F % 8 == 0 and a 16-byte aligned X.
-template <int UPW>
+// Requires F to be a whole number of 16-byte groups and a 16-byte aligned X.
+template <class Tr, int UPW>
 __global__ __launch_bounds__(kThreads, 1) void bundle_dma_kernel(
-    const bf16raw* __restrict__ X, const uint4* __restrict__ Bp, const int32_t* __restrict__ y,
-    int32_t* __restrict__ counts, int N, int F, int D, int K, int ndb, int ngroups) {
-  typedef TrBF16 Tr;
+    const typename Tr::elem* __restrict__ X, const uint4* __restrict__ Bp,
+    const int32_t* __restrict__ y, int32_t* __restrict__ counts, int N, int F, int D, int K,
+    int ndb, int ngroups) {
+  typedef typename Tr::elem T;
+  static_assert(Tr::kEsz <= 2, "16-byte slots of bf16 or int8");
   constexpr int NTILES = kDmaNtiles;
   constexpr int NT = 32 * NTILES;
   constexpr int kPF = UPW > 1 ? 4 : prefetch_of(NTILES, 1);
   constexpr int FSC = kDmaFsc;
   constexpr int W = 2 * FSC + 1;                 // 16-byte slots per LDS row
-  constexpr int pitch = 8 * W;                   // elements
+  constexpr int pitch = Tr::kVec * W;            // elements
   constexpr int P = dma_loads_per_wave(NTILES);  // X loads per wave per chunk
   constexpr int kDmaSteps = (P + 1) / 2;
   constexpr int kAfter = 2 * UPW * (FSC - kDmaSteps);
   constexpr int kWait = kAfter < 2 * UPW * kPF ? kAfter : 2 * UPW * kPF;
-  constexpr int buf_elems = P * kThreads * 8;
+  constexpr int buf_elems = P * kThreads * Tr::kVec;
   constexpr int kCols = kWaves * UPW * 64;  // columns per workgroup
+  constexpr int kTileBytes = 32 * pitch * Tr::kEsz;     // 32 rows of a buffer
+  constexpr int kStepBytes = Tr::kFStep * Tr::kEsz;     // one f-step of a row
   static_assert(NT == 64 && FSC % kPF == 0 && kDmaSteps <= FSC && kWait <= 63, "schedule");
   constexpr int kWaitImm = 0x0F70 | (kWait & 15) | ((kWait >> 4) << 14);
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
@@ -1463,9 +1467,9 @@ __global__ __launch_bounds__(kThreads, 1) void bundle_dma_kernel(
   const int t_end = (int)((int64_t)ntiles * (sg + 1) / ngroups);
 
   // LDS: [two X buffers | zero slot | labels 2 x NT | counters K x kCols]
-  bf16raw* xb = reinterpret_cast<bf16raw*>(lds);
-  const bf16raw* xzero = xb + 2 * buf_elems;
-  int* ys = reinterpret_cast<int*>(xb + 2 * buf_elems + 8);
+  T* xb = reinterpret_cast<T*>(lds);
+  const T* xzero = xb + 2 * buf_elems;
+  int* ys = reinterpret_cast<int*>(lds + 2 * buf_elems * sizeof(T) + 16);
   int* cnt = ys + 2 * NT;
   if (tid == 0) *reinterpret_cast<uint4*>(xb + 2 * buf_elems) = make_uint4(0u, 0u, 0u, 0u);
   for (int i = tid; i < K * kCols; i += kThreads) cnt[i] = 0;
@@ -1476,17 +1480,17 @@ __global__ __launch_bounds__(kThreads, 1) void bundle_dma_kernel(
     const int64_t n0 = (int64_t)tl * NT;
     const int rows = (int)min((int64_t)NT, (int64_t)N - n0);
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<bf16raw*>(X + n0 * F), 0, rows * F * 2, 0x00020000);
+        const_cast<T*>(X + n0 * F), 0, rows * F * Tr::kEsz, 0x00020000);
     int q = (p * kWaves + wave) * 64 + lane;
     asm volatile("" : "+v"(q));
     const int r = q / W, rem = q - r * W;
-    const int col = (ch * FSC + (rem >> 1)) * 16 + (rem & 1) * 8;
+    const int col = (ch * FSC + (rem >> 1)) * Tr::kFStep + (rem & 1) * Tr::kVec;
     const bool ok = r < rows && rem < 2 * FSC && col < F;
-    const unsigned off = ok ? (unsigned)((r * F + col) * 2) : 0x80000000u;
+    const unsigned off = ok ? (unsigned)((r * F + col) * Tr::kEsz) : 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         xr,
         (__attribute__((address_space(3))) void*)(xb + buf * buf_elems +
-                                                  (p * kWaves + wave) * 64 * 8),
+                                                  (p * kWaves + wave) * 64 * Tr::kVec),
         16, off, 0, 0, 0);
   };
   // The labels of tile tl into label buffer tl & 1 (lane l: row l).
@@ -1559,7 +1563,7 @@ __global__ __launch_bounds__(kThreads, 1) void bundle_dma_kernel(
       const int nbuf = cur ^ 1;
       uint4 xfr[2][NTILES];
 #pragma unroll
-      for (int t = 0; t < NTILES; ++t) xfr[0][t] = lds_read16_issue(xc + t * 64 * pitch);
+      for (int t = 0; t < NTILES; ++t) xfr[0][t] = lds_read16_issue(xc + t * kTileBytes);
 #pragma unroll
       for (int s = 0; s < FSC; ++s) {
         const int i = s % kPF;
@@ -1567,7 +1571,7 @@ __global__ __launch_bounds__(kThreads, 1) void bundle_dma_kernel(
 #pragma unroll
         for (int t = 0; t < NTILES; ++t)
           xfr[(s + 1) & 1][t] =
-              lds_read16_issue(s + 1 < fsn ? xc + t * 64 * pitch + (s + 1) * 32 : xz);
+              lds_read16_issue(s + 1 < fsn ? xc + t * kTileBytes + (s + 1) * kStepBytes : xz);
 #pragma unroll
         for (int j = 0; j < UPW; ++j)
 #pragma unroll
@@ -1808,7 +1812,7 @@ BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true
   if (K < 1 || K > kBundleMfmaMaxK || F > (1 << 20) || N > (1 << 30) || N < 1) return c;
   if (Tr::kEsz == 1 && F > kI8MaxF) return c;
   if (cdiv(D, 64) * 2 * nfs_of<Tr>((int)F) * 1024 >= ((int64_t)1 << 31)) return c;
-  if (Tr::kEsz == 2 && F % 8 == 0 && x16) {
+  if (Tr::kEsz <= 2 && F % Tr::kVec == 0 && x16) {
     // double-buffered kernel: two units per wave while the class counters fit
     const size_t base = (size_t)2 * dma_loads_per_wave(kDmaNtiles) * kThreads * 16 + 16 +
                         sizeof(int) * 2 * 32 * kDmaNtiles;
@@ -1831,8 +1835,8 @@ BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true
       }
     }
   }
-  c.nt = Tr::kEsz <= 2 ? 4 : 2;
-  c.occ = Tr::kEsz <= 2 ? 1 : 2;
+  c.nt = Tr::kEsz == 1 ? 4 : 2;
+  c.occ = Tr::kEsz == 1 ? 1 : 2;
   const int nfs = nfs_of<Tr>((int)F);
   const int pad = pad_of<Tr>();
   const size_t fixed = 16 + sizeof(int) * (32 * c.nt + (size_t)K * kBundleCols);
@@ -1857,6 +1861,28 @@ BundleCfg bundle_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true
   return c;
 }
 
+template <class Tr>
+hipError_t launch_bundle_dma(const BundleCfg& c, const void* X, const void* packed,
+                             const int32_t* y, int32_t* counts, int64_t N, int64_t F, int64_t D,
+                             int64_t K, int ndb, hipStream_t stream) {
+  typedef typename Tr::elem T;
+  const dim3 grid((unsigned)(c.ncg * c.ngroups)), block(kThreads);
+  if (c.dma_upw == 2) {
+    const hipError_t a = allow_large_lds<&bundle_dma_kernel<Tr, 2>>();
+    if (a != hipSuccess) return a;
+    hipLaunchKernelGGL((bundle_dma_kernel<Tr, 2>), grid, block, c.lds, stream, (const T*)X,
+                       (const uint4*)packed, y, counts, (int)N, (int)F, (int)D, (int)K, ndb,
+                       c.ngroups);
+  } else {
+    const hipError_t a = allow_large_lds<&bundle_dma_kernel<Tr, 1>>();
+    if (a != hipSuccess) return a;
+    hipLaunchKernelGGL((bundle_dma_kernel<Tr, 1>), grid, block, c.lds, stream, (const T*)X,
+                       (const uint4*)packed, y, counts, (int)N, (int)F, (int)D, (int)K, ndb,
+                       c.ngroups);
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
 
 bool bundle_packed_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
@@ -1865,7 +1891,11 @@ bool bundle_packed_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt)
 
 const char* bundle_packed_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   if (dt == 0) return bundle_cfg<TrF32>(N, F, D, K).ok ? "bundle_mfma_kernel" : "";
-  if (dt == 2) return bundle_cfg<TrI8>(N, F, D, K).ok ? "bundle_mfma_kernel" : "";
+  if (dt == 2) {
+    const BundleCfg c = bundle_cfg<TrI8>(N, F, D, K);
+    if (!c.ok) return "";
+    return c.dma_upw > 0 ? "bundle_dma_kernel" : "bundle_mfma_kernel";
+  }
   const BundleCfg c = bundle_cfg<TrBF16>(N, F, D, K);
   if (!c.ok) return "";
   return c.dma_upw > 0 ? "bundle_dma_kernel" : "bundle_mfma_kernel";
@@ -1886,9 +1916,11 @@ hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t
                        (const float*)X, (const uint4*)packed, y, counts, (int)N, (int)F, (int)D,
                        (int)K, g.ndb, c.ngroups, c.fsc);
   } else if (dt == 2) {
-    const BundleCfg c = bundle_cfg<TrI8>(N, F, D, K);
+    const BundleCfg c = bundle_cfg<TrI8>(N, F, D, K, ((uintptr_t)X % 16) == 0);
     if (!c.ok) return hipErrorInvalidValue;
     const PackGeom g = pack_geom<TrI8>(F, D, 1);
+    if (c.dma_upw > 0)
+      return launch_bundle_dma<TrI8>(c, X, packed, y, counts, N, F, D, K, g.ndb, stream);
     auto* k = &bundle_mfma_kernel<TrI8, 4, 1>;
     const hipError_t a = allow_large_lds<&bundle_mfma_kernel<TrI8, 4, 1>>();
     if (a != hipSuccess) return a;
@@ -1899,25 +1931,10 @@ hipError_t launch_bundle_packed(const void* X, const void* packed, const int32_t
     const BundleCfg c = bundle_cfg<TrBF16>(N, F, D, K, ((uintptr_t)X % 16) == 0);
     if (!c.ok) return hipErrorInvalidValue;
     const PackGeom g = pack_geom<TrBF16>(F, D, 1);
-    if (c.dma_upw > 0) {
-      const dim3 grid((unsigned)(c.ncg * c.ngroups));
-      if (c.dma_upw == 2) {
-        const hipError_t a = allow_large_lds<&bundle_dma_kernel<2>>();
-        if (a != hipSuccess) return a;
-        hipLaunchKernelGGL(bundle_dma_kernel<2>, grid, block, c.lds, stream, (const bf16raw*)X,
-                           (const uint4*)packed, y, counts, (int)N, (int)F, (int)D, (int)K,
-                           g.ndb, c.ngroups);
-      } else {
-        const hipError_t a = allow_large_lds<&bundle_dma_kernel<1>>();
-        if (a != hipSuccess) return a;
-        hipLaunchKernelGGL(bundle_dma_kernel<1>, grid, block, c.lds, stream, (const bf16raw*)X,
-                           (const uint4*)packed, y, counts, (int)N, (int)F, (int)D, (int)K,
-                           g.ndb, c.ngroups);
-      }
-      return hipGetLastError();
-    }
-    auto* k = &bundle_mfma_kernel<TrBF16, 4, 1>;
-    const hipError_t a = allow_large_lds<&bundle_mfma_kernel<TrBF16, 4, 1>>();
+    if (c.dma_upw > 0)
+      return launch_bundle_dma<TrBF16>(c, X, packed, y, counts, N, F, D, K, g.ndb, stream);
+    auto* k = &bundle_mfma_kernel<TrBF16, 2, 2>;
+    const hipError_t a = allow_large_lds<&bundle_mfma_kernel<TrBF16, 2, 2>>();
     if (a != hipSuccess) return a;
     hipLaunchKernelGGL(k, dim3((unsigned)(c.ncg * c.ngroups)), block, c.lds, stream,
                        (const bf16raw*)X, (const uint4*)packed, y, counts, (int)N, (int)F,

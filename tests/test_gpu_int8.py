@@ -113,13 +113,16 @@ def test_int8_largest_d(hd):
     check(y, S, oracle.infer(X, B, C))
 
 
-def test_int8_training_and_round_trip(hd):
+@pytest.mark.parametrize("N,F,D,K,kernel", [(2000, 617, 4096, 26, "bundle_mfma_kernel"),
+                                             (1500, 3072, 2000, 26, "bundle_dma_kernel"),
+                                             (130, 4096, 700, 60, "bundle_dma_kernel")])
+def test_int8_training_and_round_trip(hd, N, F, D, K, kernel):
     """Single-pass training from int8 samples (exact class sums), then the
     codebook as an int8 model: a class with one sample scores exactly D on
     that sample."""
     torch = torch_or_skip()
-    N, F, D, K = 2000, 617, 4096, 26
-    announce(f"int8 training N={N} F={F} D={D} K={K}")
+    assert hd.bundle_kernel(N, F, D, K, torch.int8, packed=True) == kernel
+    announce(f"int8 training N={N} F={F} D={D} K={K} ({kernel})")
     X, B, _ = hd_inputs.make_int8_inputs(N, F, D, 1, seed=11)
     y = np.random.default_rng(11).integers(0, K, N).astype(np.int32)
     y[:K] = np.arange(K)
