@@ -81,6 +81,19 @@ typedef enum { HD_F32 = 0, HD_BF16 = 1, HD_I8 = 2 } hd_dtype;
  * HD_ACT_IDENTITY skips it (H = X B): a linear test mode, S = X B C^T. */
 typedef enum { HD_ACT_HARDSIGN = 0, HD_ACT_IDENTITY = 1 } hd_act;
 
+/*
+ * Flag OR-ed into the act argument of hd_infer, hd_infer_packed and
+ * hd_infer_packed_noalloc: scores and labels identical bit for bit from call
+ * to call for the same inputs (the split of D of Sec. III-C Alg. 3 otherwise
+ * sums partial scores with fp32 atomics in arrival order, which can change
+ * their low bits, and so a near-tie label, between calls). The small-batch
+ * path then gives each workgroup its own partial-score slot and sums the
+ * slots in a fixed order; the large-batch path already sums in a fixed
+ * order. The workspace size queries cover this mode. Not supported by
+ * hd_infer_stream (HD_ERR_UNSUPPORTED).
+ */
+#define HD_DETERMINISTIC 0x100
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *hd_status_str(hd_status s);
 

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(PKG, "libhd.so")
 
 HD_OK, HD_ERR_ARG, HD_ERR_UNSUPPORTED, HD_ERR_WORKSPACE, HD_ERR_HIP = range(5)
 HD_F32, HD_BF16, HD_I8 = 0, 1, 2
+HD_DETERMINISTIC = 0x100  # flag OR-ed into act: bit-identical results from call to call
 ACTS = {"hardsign": 0, "identity": 1}
 
 SYMBOLS = (
@@ -212,9 +213,16 @@ def infer_kernel(N: int, F: int, D: int, K: int, dtype, packed: bool = True) -> 
     return lib().hd_infer_kernel(N, F, D, K, dt, 1 if packed else 0).decode()
 
 
+def _act(act: str, deterministic: bool) -> int:
+    return ACTS[act] | (HD_DETERMINISTIC if deterministic else 0)
+
+
 def infer(X, B, C, act: str = "hardsign", return_scores: bool = False, out=None,
-          workspace=None):
+          workspace=None, deterministic: bool = False):
     """Alg. 1 fused: labels[N] int32 (and scores[N, K] float32).
+
+    ``deterministic``: bit-identical scores and labels from call to call
+    (fixed-order reduction of the partial scores).
 
     ``out`` may be a (labels, scores-or-None) pair of preallocated tensors.
     ``workspace`` may be a zeroed uint8 device tensor of at least
@@ -240,7 +248,8 @@ def infer(X, B, C, act: str = "hardsign", return_scores: bool = False, out=None,
     need = int(L.hd_infer_workspace_bytes(N, F, D, K, dt))
     ws = workspace if workspace is not None else _workspace(X.device, need, ("infer", N, F, D, K, dt))
     st = L.hd_infer(X.data_ptr(), B.data_ptr(), C.data_ptr(), labels.data_ptr(),
-                    scores.data_ptr() if scores is not None else None, N, F, D, K, dt, ACTS[act],
+                    scores.data_ptr() if scores is not None else None, N, F, D, K, dt,
+                    _act(act, deterministic),
                     ws.data_ptr() if ws is not None else None,
                     ws.numel() if ws is not None else 0, _stream_ptr(X.device))
     _raise(st, "hd_infer")
@@ -279,7 +288,7 @@ def pack_model(B, C=None, K: int = 1) -> PackedModel:
 
 
 def infer_packed(X, model: PackedModel, act: str = "hardsign", return_scores: bool = False,
-                 out=None, workspace=None):
+                 out=None, workspace=None, deterministic: bool = False):
     """Alg. 1 fused from a packed model: labels[N] (and scores[N, K])."""
     torch = _torch()
     _check_dev(X)
@@ -301,14 +310,14 @@ def infer_packed(X, model: PackedModel, act: str = "hardsign", return_scores: bo
                                                             ("packed", N, F, D, K, dt))
     st = L.hd_infer_packed(X.data_ptr(), model.image.data_ptr(), labels.data_ptr(),
                            scores.data_ptr() if scores is not None else None, N, F, D, K, dt,
-                           ACTS[act], ws.data_ptr() if ws is not None else None,
+                           _act(act, deterministic), ws.data_ptr() if ws is not None else None,
                            ws.numel() if ws is not None else 0, _stream_ptr(X.device))
     _raise(st, "hd_infer_packed")
     return (labels, scores) if (return_scores or out is not None) else labels
 
 
 def infer_packed_noalloc(X, model: PackedModel, act: str = "hardsign", return_scores: bool = False,
-                         out=None):
+                         out=None, deterministic: bool = False):
     """``infer_packed`` on the library's fixed scratch (no workspace argument;
     calls on one GPU must not overlap in time)."""
     torch = _torch()
@@ -327,7 +336,7 @@ def infer_packed_noalloc(X, model: PackedModel, act: str = "hardsign", return_sc
                   if return_scores else None)
     st = lib().hd_infer_packed_noalloc(X.data_ptr(), model.image.data_ptr(), labels.data_ptr(),
                                        scores.data_ptr() if scores is not None else None, N, F, D,
-                                       K, dt, ACTS[act], _stream_ptr(X.device))
+                                       K, dt, _act(act, deterministic), _stream_ptr(X.device))
     _raise(st, "hd_infer_packed_noalloc")
     return (labels, scores) if (return_scores or out is not None) else labels
 

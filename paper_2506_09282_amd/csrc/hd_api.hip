@@ -21,6 +21,11 @@ bool enums_ok(int dt, int act) {
 // with the HardSign activation.
 bool i8_ok(int dt, int act) { return dt != HD_I8 || act == 0; }
 
+// The act argument of the inference calls: an hd_act, optionally OR-ed with
+// HD_DETERMINISTIC.
+int act_base(int act) { return act & ~HD_DETERMINISTIC; }
+bool det_of(int act) { return (act & HD_DETERMINISTIC) != 0; }
+
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 // Path choice. The split-D small-batch path serves small batches whenever its
@@ -141,21 +146,31 @@ size_t hd_model_packed_bytes(int64_t F, int64_t D, int64_t K, hd_dtype dt) {
   return image_layout(F, D, K, dt).total;
 }
 
-size_t hd_infer_packed_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
-  if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
-  const Route r = route(N, F, D, K, dt, true);
+// Workspace one call needs: with a packed model or raw matrices, in the
+// default or the deterministic mode (the size queries cover both modes).
+static size_t workspace_need(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool packed,
+                             bool det) {
+  const Route r = route(N, F, D, K, dt, packed);
   if (r == Route::kSmall || r == Route::kSmallChunked)
-    return hd::small_workspace_bytes(small_n(r, N), F, D, K, dt);
-  return hd::large_workspace_bytes(N, F, D, K, dt);
+    return hd::small_workspace_bytes(small_n(r, N), F, D, K, dt, det);
+  if (packed) return hd::large_workspace_bytes(N, F, D, K, dt);
+  return align256(hd::large_workspace_bytes(N, F, D, K, dt)) +
+         align256(hd::large_packed_bytes(F, D, K, dt));
+}
+
+static size_t workspace_query(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool packed) {
+  if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
+  const size_t a = workspace_need(N, F, D, K, dt, packed, false);
+  const size_t b = workspace_need(N, F, D, K, dt, packed, true);
+  return a > b ? a : b;
+}
+
+size_t hd_infer_packed_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
+  return workspace_query(N, F, D, K, dt, true);
 }
 
 size_t hd_infer_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt) {
-  if (N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, 0) || !dims_ok(N, F, D, K)) return 0;
-  const Route r = route(N, F, D, K, dt, false);
-  if (r == Route::kSmall || r == Route::kSmallChunked)
-    return hd::small_workspace_bytes(small_n(r, N), F, D, K, dt);
-  return align256(hd::large_workspace_bytes(N, F, D, K, dt)) +
-         align256(hd::large_packed_bytes(F, D, K, dt));
+  return workspace_query(N, F, D, K, dt, false);
 }
 
 hd_status hd_pack_model(const void* B, const void* C, int64_t F, int64_t D, int64_t K, hd_dtype dt,
@@ -177,20 +192,21 @@ hd_status hd_pack_model(const void* B, const void* C, int64_t F, int64_t D, int6
 // enqueueing nothing.
 static hd_status infer_common(const void* X, const void* B, const void* C, const void* packed,
                               int32_t* labels, float* scores, int64_t N, int64_t F, int64_t D,
-                              int64_t K, hd_dtype dt, hd_act act, void* workspace,
+                              int64_t K, hd_dtype dt, int act, void* workspace,
                               size_t workspace_bytes, hipStream_t stream, bool dry = false) {
-  if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
-  if (!dims_ok(N, F, D, K) || !i8_ok(dt, act)) return HD_ERR_UNSUPPORTED;
+  if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act_base(act))) return HD_ERR_ARG;
+  if (!dims_ok(N, F, D, K) || !i8_ok(dt, act_base(act))) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
   if (!X || !labels || (packed ? false : (!B || !C))) return HD_ERR_ARG;
+  const bool det = det_of(act);
+  act = act_base(act);
   const size_t es = esize(dt);
   if (!aligned(X, es) || !aligned(labels, 4) || !aligned(scores, 4) || !aligned(workspace, 256) ||
       (packed ? !aligned(packed, 256) : (!aligned(B, es) || !aligned(C, es))))
     return HD_ERR_ARG;
   const Route r = route(N, F, D, K, dt, packed != nullptr);
   if (r == Route::kNone) return HD_ERR_UNSUPPORTED;
-  const size_t need = packed ? hd_infer_packed_workspace_bytes(N, F, D, K, dt)
-                             : hd_infer_workspace_bytes(N, F, D, K, dt);
+  const size_t need = workspace_need(N, F, D, K, dt, packed != nullptr, det);
   if (need > 0 && !workspace) return HD_ERR_ARG;
   if (workspace_bytes < need) return HD_ERR_WORKSPACE;
 
@@ -202,7 +218,8 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
       const int64_t n = N - n0 < step ? N - n0 : step;
       const hipError_t e = hd::launch_small(
           static_cast<const char*>(X) + n0 * F * (int64_t)es, B, C, packed != nullptr,
-          labels + n0, scores ? scores + n0 * K : nullptr, n, F, D, K, dt, act, workspace, stream);
+          labels + n0, scores ? scores + n0 * K : nullptr, n, F, D, K, dt,
+          act | (det ? hd::kSmallActDet : 0), workspace, stream);
       if (e != hipSuccess) return HD_ERR_HIP;
     }
     return HD_OK;
@@ -269,7 +286,9 @@ hd_status hd_infer_stream(const void* X, const void* packed, const uint32_t* rea
                           int32_t* labels, float* scores, uint32_t* done, int64_t nbatch,
                           int64_t N, int64_t F, int64_t D, int64_t K, hd_dtype dt, hd_act act,
                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (nbatch < 0 || N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
+  if (nbatch < 0 || N < 1 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act_base(act)))
+    return HD_ERR_ARG;
+  if (det_of(act)) return HD_ERR_UNSUPPORTED;
   if (!dims_ok(N, F, D, K) || nbatch > kMaxDim || nbatch * N > kMaxDim)
     return HD_ERR_UNSUPPORTED;
   if (nbatch == 0) return HD_OK;
@@ -361,10 +380,10 @@ hd_status hd_infer_packed_noalloc(const void* X, const void* packed, int32_t* la
                                   float* scores, int64_t N, int64_t F, int64_t D, int64_t K,
                                   hd_dtype dt, hd_act act, hipStream_t stream) {
   if (N > 0 && !packed) return HD_ERR_ARG;
-  if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act)) return HD_ERR_ARG;
-  if (!dims_ok(N, F, D, K)) return HD_ERR_UNSUPPORTED;
+  if (N < 0 || F < 1 || D < 1 || K < 1 || !enums_ok(dt, act_base(act))) return HD_ERR_ARG;
+  if (!dims_ok(N, F, D, K) || !i8_ok(dt, act_base(act))) return HD_ERR_UNSUPPORTED;
   if (N == 0) return HD_OK;
-  const size_t need = hd_infer_packed_workspace_bytes(N, F, D, K, dt);
+  const size_t need = workspace_need(N, F, D, K, dt, true, det_of(act));
   if (need > kScratchBytes) return HD_ERR_WORKSPACE;
   void* ws = nullptr;
   // every check of the allocating entry point, before anything is enqueued

@@ -39,7 +39,11 @@ constexpr int kSmallMaxN = 64;
 constexpr int kSmallReplicas = 32;  // replicated score accumulators
 
 bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
-size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt);
+// `act` of launch_small: bit 0 the activation, bit 1 the deterministic reduction.
+constexpr int kSmallActDet = 2;
+// Workspace of the small-batch kernels; det: the deterministic reduction (one
+// score replica per workgroup plus one per ticket group).
+size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool det);
 // Name of the kernel launch_small would use for 16-byte aligned operands.
 // Whether the small-batch plan for these sizes (16-byte aligned operands)
 // runs on the matrix cores rather than the VALU fallback.

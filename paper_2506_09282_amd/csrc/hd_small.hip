@@ -242,8 +242,10 @@ bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
   return plan_valu(N, F, D, K, 8).nb > 0;
 }
 
-size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
-  return (size_t)kLine * (1 + kGroups) + sizeof(float) * (size_t)kSmallReplicas * N * K;
+size_t small_workspace_bytes(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool det) {
+  // every plan's grid is at most one workgroup per column block
+  const int64_t slots = det ? cdiv(D, kW) + kGroups : kSmallReplicas;
+  return (size_t)kLine * (1 + kGroups) + sizeof(float) * (size_t)slots * N * K;
 }
 
 bool small_matrix_core(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
@@ -320,6 +322,7 @@ hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled,
   }
   SmallPlan p = plan_small(N, F, D, K, dt, lay, (uintptr_t)X % 16 == 0);
   if (p.nb == 0) return hipErrorInvalidValue;
+  if ((act & kActDet) && p.grid > cdiv(D, kW)) return hipErrorInvalidValue;  // workspace bound
   const Args a{X, B, C, labels, scores, (int)N, (int)F, (int)D, (int)K, act, workspace, stream};
   if (p.frag) {
     if (!frag) return hipErrorInvalidValue;

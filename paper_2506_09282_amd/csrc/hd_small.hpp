@@ -208,11 +208,106 @@ __device__ void block_scores(const ColView<T, LAY>& cv, const float* hs, float* 
 // counter b % kGroups; the group's last drawer (which then knows that every
 // member's partials are performed) resets it and draws from the final
 // counter; the last of those finishes.
+//
+// Deterministic mode (det, with R == G: one replica per workgroup): every
+// replica slot receives exactly one add onto zero, so it holds that
+// workgroup's partial exactly, and the sums are taken in a fixed order: the
+// group's last drawer sums its members' slots in member order into the
+// group's slot (after the G replicas), and the final workgroup sums the group
+// slots in group order. Scores and labels are then identical from run to run.
+template <int NT>
+__device__ void finish_deterministic(int N, int K, const SmallWs& ws,
+                                     int32_t* __restrict__ labels, float* __restrict__ scores,
+                                     float* buf, int buf_floats, int* s_last) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int kB = 32;  // slots read per batch (independent atomics in flight)
+  const unsigned G = gridDim.x, ng = G < kGroups ? G : kGroups, g = blockIdx.x % ng;
+  const unsigned gsize = G / ng + (g < G % ng ? 1u : 0u);
+  const int64_t NK = (int64_t)N * K;
+  float* gacc = ws.sacc + (int64_t)G * NK;
+  // sum of `count` slots base[j * stride + o] in order j = 0, 1, ...
+  auto ordered_sum = [&](const float* base, int64_t stride, unsigned count, int64_t o) {
+    float s = 0.0f;
+    for (unsigned j0 = 0; j0 < count; j0 += kB) {
+      float t[kB];
+#pragma unroll
+      for (int j = 0; j < kB; ++j)
+        t[j] = j0 + j < count ? take_and_clear(const_cast<float*>(base) + (j0 + j) * stride + o)
+                              : 0.0f;
+#pragma unroll
+      for (int j = 0; j < kB; ++j)
+        if (j0 + j < count) s += t[j];
+    }
+    return s;
+  };
+  if (tid == 0) {
+    unsigned* gc = ws.group + g * (kLine / 4);
+    const int last = take_ticket(gc) == gsize - 1 ? 1 : 0;
+    if (last) reset_counter(gc);
+    *s_last = last;
+  }
+  __syncthreads();
+  if (!*s_last) return;
+  // group g's members are workgroups g, g + ng, g + 2 ng, ...
+  for (int64_t o = tid; o < NK; o += NT)
+    publish_store(gacc + (int64_t)g * NK + o,
+                  ordered_sum(ws.sacc + (int64_t)g * NK, (int64_t)ng * NK, gsize, o));
+  wait_own_memory_ops();
+  __syncthreads();
+  if (tid == 0) *s_last = take_ticket(ws.counter) == ng - 1 ? 1 : 0;
+  __syncthreads();
+  if (!*s_last) return;
+  if (NK <= buf_floats) {
+    for (int64_t o = tid; o < NK; o += NT) {
+      const float s = ordered_sum(gacc, NK, ng, o);
+      buf[o] = s;
+      if (scores) scores[o] = s;
+    }
+    __syncthreads();
+    for (int n = tid; n < N; n += NT) {
+      float best = buf[(int64_t)n * K];
+      int best_k = 0;
+      for (int k = 1; k < K; ++k) {
+        const float s = buf[(int64_t)n * K + k];
+        if (s > best) {
+          best = s;
+          best_k = k;
+        }
+      }
+      labels[n] = best_k;
+    }
+  } else {
+    for (int n = wave; n < N; n += NT / kWave) {
+      float best = -__builtin_huge_valf();
+      int best_k = 0x7fffffff;
+      for (int k = lane; k < K; k += kWave) {
+        const float s = ordered_sum(gacc, NK, ng, (int64_t)n * K + k);
+        if (scores) scores[(int64_t)n * K + k] = s;
+        if (k == lane || s > best) {
+          best = s;
+          best_k = k;
+        }
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const float ob = __shfl_xor(best, off, kWave);
+        const int ok = __shfl_xor(best_k, off, kWave);
+        if (ob > best || (ob == best && ok < best_k)) {
+          best = ob;
+          best_k = ok;
+        }
+      }
+      if (lane == 0) labels[n] = best_k;
+    }
+  }
+  if (tid == 0) reset_counter(ws.counter);
+}
+
 template <int NT = kThreads>
 __device__ void publish_and_finish(const float* sl, int nb0, int nb, int N, int K, int R,
                                    const SmallWs& ws, int32_t* __restrict__ labels,
                                    float* __restrict__ scores, float* buf, int buf_floats,
-                                   bool finish) {
+                                   bool finish, bool det) {
   const int tid = threadIdx.x;
   float* my = ws.sacc + (int64_t)(blockIdx.x % R) * N * K;
   for (int p = tid; p < nb * K; p += NT) publish_add(my + (int64_t)nb0 * K + p, sl[p]);
@@ -220,6 +315,10 @@ __device__ void publish_and_finish(const float* sl, int nb0, int nb, int N, int 
   __shared__ int s_last;
   wait_own_memory_ops();
   __syncthreads();
+  if (det) {
+    finish_deterministic<NT>(N, K, ws, labels, scores, buf, buf_floats, &s_last);
+    return;
+  }
   if (tid == 0) {
     const unsigned G = gridDim.x, ng = G < kGroups ? G : kGroups, g = blockIdx.x % ng;
     const unsigned gsize = G / ng + (g < G % ng ? 1u : 0u);
@@ -379,6 +478,10 @@ hipError_t allow_lds() {
                                hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget);
   });
 }
+
+// Kernel argument `act` of the small-batch kernels: bit 0 the activation
+// (1 = identity), bit 1 the deterministic reduction.
+constexpr int kActDet = kSmallActDet;
 
 struct Args {
   const void *X, *B, *C;

@@ -28,7 +28,9 @@ __global__ __launch_bounds__(kThreads) void small_flat_kernel(
   const int cg = tid % kCG, rg = tid / kCG;
   const int G = gridDim.x;
   const int blk = xcd_block(blockIdx.x, G);
-  const int R = replicas(G, N * K);
+  const bool det = (act & kActDet) != 0;
+  act &= 1;
+  const int R = det ? G : replicas(G, N * K);
   const int64_t d0 = (int64_t)blk * kW;
   const int npairs = N * K;
 
@@ -101,7 +103,8 @@ __global__ __launch_bounds__(kThreads) void small_flat_kernel(
     publish_add(my + p, sc);
   }
   float none[1] = {0.0f};
-  publish_and_finish(none, 0, 0, N, K, R, ws, labels, scores, red, kWaves * 4 * NB * kW, true);
+  publish_and_finish(none, 0, 0, N, K, R, ws, labels, scores, red, kWaves * 4 * NB * kW, true,
+                     det);
 }
 
 

@@ -56,7 +56,9 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
   const int cw = wave - kWaves;  // compute wave index
   const int G = gridDim.x;
   const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
-  const int R = replicas(G, N * K);
+  const bool det = (act & kActDet) != 0;
+  act &= 1;
+  const int R = det ? G : replicas(G, N * K);
   const int nb = min(NB, N);
   const int npairs = nb * K;
   const int nmine = walk.count();
@@ -244,7 +246,7 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
   }
   __syncthreads();
   publish_and_finish<kFragThreads>(sl, 0, nb, N, K, R, ws, labels, scores, smem, lds_floats,
-                                   true);
+                                   true, det);
 }
 
 // Writes the fragment section: out[((blk*4 + w)*(MS/4) + g)*64 + l][e] =

@@ -39,7 +39,9 @@ __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = gridDim.x;
   const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
-  const int R = replicas(G, N * K);
+  const bool det = (act & kActDet) != 0;
+  act &= 1;
+  const int R = det ? G : replicas(G, N * K);
   const int nb = min(NB, N);
   const int npairs = nb * K;
   const int arow = wave * FQ + (lane >> 4);  // A-operand row of step 0
@@ -107,7 +109,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_mfma_kernel(
 
   ring3_run(nmine, b0, b1, b2, load, process);
   __syncthreads();
-  publish_and_finish(sl, 0, nb, N, K, R, ws, labels, scores, smem, lds_floats, true);
+  publish_and_finish(sl, 0, nb, N, K, R, ws, labels, scores, smem, lds_floats, true, det);
 }
 
 
@@ -137,7 +139,9 @@ __global__ __launch_bounds__(kThreads) void small_block_mfma_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = gridDim.x;
   const int blk = xcd_block(blockIdx.x, G);
-  const int R = replicas(G, N * K);
+  const bool det = (act & kActDet) != 0;
+  act &= 1;
+  const int R = det ? G : replicas(G, N * K);
   const int nb = min(NB, N);
   const int npairs = nb * K;
   const int arow = wave * FQ + (lane >> 4);
@@ -229,7 +233,7 @@ __global__ __launch_bounds__(kThreads) void small_block_mfma_kernel(
     publish_add(my + p, sc);
   }
   float none[1] = {0.0f};
-  publish_and_finish(none, 0, 0, N, K, R, ws, labels, scores, smem, lds_floats, true);
+  publish_and_finish(none, 0, 0, N, K, R, ws, labels, scores, smem, lds_floats, true, det);
 }
 
 

@@ -38,7 +38,9 @@ __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
   const int cg = tid % kCG, rg = tid / kCG;
   const int G = gridDim.x;
   const BlockWalk walk = block_walk(blockIdx.x, G, nblocks);
-  const int R = replicas(G, N * K);
+  const bool det = (act & kActDet) != 0;
+  act &= 1;
+  const int R = det ? G : replicas(G, N * K);
   const int nmine = walk.count();
   const int nitems = nmine * nchunks;
 
@@ -144,7 +146,7 @@ __global__ __launch_bounds__(kThreads, 1) void small_valu_kernel(
     ring3_run(nitems, b0, b1, b2, load, process);
     __syncthreads();
     publish_and_finish(sl, nb0, nb, N, K, R, ws, labels, scores, smem, lds_floats,
-                       nb0 + NB >= N);
+                       nb0 + NB >= N, det);
   }
 }
 

@@ -45,7 +45,10 @@ def test_status_strings(L):
 def test_workspace_sizes(L):
     # small batch: 256-byte ticket header + replicated accumulators
     small = L.hd_infer_workspace_bytes(32, 561, 10240, 6, hd.HD_F32)
-    assert small == 256 * 33 + 4 * 32 * 32 * 6  # counters, then 32 score replicas
+    # counters, then the score replicas: 32 (default mode) or one per
+    # workgroup (at most one per 16-column block) plus one per ticket group
+    # (deterministic mode); the query covers both
+    assert small == 256 * 33 + 4 * max(32, 10240 // 16 + 32) * 32 * 6
     assert L.hd_infer_workspace_bytes(0, 561, 10240, 6, hd.HD_F32) == 0
     assert L.hd_infer_workspace_bytes(5, 0, 10, 6, hd.HD_F32) == 0
     # large batch, raw entry: holds the tiled model
@@ -203,3 +206,16 @@ def test_int8_limits(L):
     assert L.hd_bundle_kernel(100, 617, 4096, 26, I8, 0) == b""
     # the packed image has no small-batch section
     assert L.hd_model_packed_bytes(617, 4096, 26, I8) < L.hd_model_packed_bytes(617, 4096, 26, 1)
+
+
+def test_deterministic_flag(L):
+    """HD_DETERMINISTIC combines with either activation on the inference calls
+    and is refused by the streaming call; other bits are invalid."""
+    DET = hd.HD_DETERMINISTIC
+    assert _infer(L, N=0, X=None, labels=None, ws=None, wsb=0, act=DET) == hd.HD_OK
+    assert _infer(L, N=0, X=None, labels=None, ws=None, wsb=0, act=DET | 1) == hd.HD_OK
+    assert _infer(L, act=0x200) == hd.HD_ERR_ARG
+    assert _infer(L, act=DET | 2) == hd.HD_ERR_ARG
+    assert L.hd_infer_stream(FAKE, FAKE, None, FAKE, None, None, 1, 4, 8, 64, 3, 0, DET, FAKE,
+                             1 << 20, None) == hd.HD_ERR_UNSUPPORTED
+    assert L.hd_encode(FAKE, FAKE, FAKE, 4, 8, 16, 0, DET, None) == hd.HD_ERR_ARG
