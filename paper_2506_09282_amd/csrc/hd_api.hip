@@ -31,9 +31,10 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Path choice. The split-D small-batch path serves small batches whenever its
 // scratch fits, everything else the batch-split matrix-core path, with two
 // exceptions taken from the measured samples/s curves (F = 561, D = 10240):
-// * bf16 above 8 samples: the small-batch kernel for bf16 makes several
-//   passes over B (40 us at N = 16, 72 us at N = 32), the matrix-core path
-//   takes 34 us at N = 16..32;
+// * bf16 above 8 samples with B as given: the small-batch VALU kernel makes
+//   several passes over B (40 us at N = 16, 72 us at N = 32), the matrix-core
+//   path takes 34 us at N = 16..32; a packed bf16 model instead carries fp32
+//   fragments (bf16 widened exactly) and takes the fragment kernel;
 // * fp32 with 64 < N <= 256: the matrix-core path has only a few sample tiles
 //   (138 us for N = 65..256), while the small path takes about 32 us per 64
 //   samples, so it runs in 64-sample chunks, one after another on the stream,
@@ -46,6 +47,9 @@ Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   if (dt == HD_I8) return hd::large_supported(N, F, D, K, dt) ? Route::kLarge : Route::kNone;
   const bool small_ok = N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt);
   if (small_ok && (dt == HD_F32 || N <= kSmallMaxNBf16)) return Route::kSmall;
+  // a packed bf16 model carries fp32 fragments: the fragment kernel serves it
+  if (small_ok && dt == HD_BF16 && tiled && hd::small_matrix_core(N, F, D, K, dt, tiled))
+    return Route::kSmall;
   if (dt == HD_F32 && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
       hd::small_matrix_core(hd::kSmallMaxN, F, D, K, dt, tiled))
     return Route::kSmallChunked;

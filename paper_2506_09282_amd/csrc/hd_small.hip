@@ -77,7 +77,8 @@ int frag_ms(int64_t F) {
 }
 
 size_t frag_bytes(int64_t F, int64_t D, int dt) {
-  const int ms = dt == 0 ? frag_ms(F) : 0;
+  // fp32 fragments for fp32 and bf16 models (bf16 B widened exactly)
+  const int ms = dt <= 1 ? frag_ms(F) : 0;
   return (size_t)cdiv(D, kW) * 256 * ms * sizeof(float);
 }
 
@@ -92,7 +93,7 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay
   if (v.nb == 0) return v;
   SmallPlan p{};
   p.nblocks = v.nblocks;
-  if (lay == kTiled && dt == 0 && x_aligned && N > 8 && frag_ms(F) > 0) {
+  if (lay == kTiled && dt <= 1 && x_aligned && N > 8 && frag_ms(F) > 0) {
     const int nti = (int)cdiv(N, 16), ms = frag_ms(F);
     const int64_t nbk = 16 * nti;
     int64_t cslots = 1;  // the most blocks any workgroup walks
@@ -280,7 +281,7 @@ hipError_t launch_pack_small(const void* B, const void* C, int64_t F, int64_t D,
                                : pack_small_t<bf16raw>(B, C, F, D, K, out, stream);
   if (e != hipSuccess || frag_bytes(F, D, dt) == 0) return e;
   return launch_pack_frag(B, static_cast<char*>(out) + small_tiles_bytes(F, D, K, dt), F, D,
-                          cdiv(D, kW), frag_ms(F), stream);
+                          cdiv(D, kW), frag_ms(F), dt, stream);
 }
 
 bool stream_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
@@ -326,7 +327,7 @@ hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled,
   const Args a{X, B, C, labels, scores, (int)N, (int)F, (int)D, (int)K, act, workspace, stream};
   if (p.frag) {
     if (!frag) return hipErrorInvalidValue;
-    return launch_frag_family(p, a, frag);
+    return launch_frag_family(p, a, frag, dt);
   }
   return launch_plan(p, a, dt, lay);
 }

@@ -535,9 +535,9 @@ hipError_t launch_valu_family(SmallPlan& p, const Args& a, int dt, int lay);
 hipError_t launch_flat_family(const SmallPlan& p, const Args& a, int dt, int lay);
 hipError_t launch_mfma_family(SmallPlan& p, const Args& a, int lay);
 hipError_t launch_bmfma_family(SmallPlan& p, const Args& a, int lay);
-hipError_t launch_frag_family(SmallPlan& p, const Args& a, const void* frag);
+hipError_t launch_frag_family(SmallPlan& p, const Args& a, const void* frag, int dt);
 hipError_t launch_pack_frag(const void* B, void* out, int64_t F, int64_t D, int64_t nblk, int ms,
-                            hipStream_t stream);
+                            int dt, hipStream_t stream);
 
 }  // namespace sp
 }  // namespace hd

@@ -7,7 +7,9 @@ namespace sp {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Fragment matrix-core kernel (fp32, 8 < N <= 64, packed model). The packed
+// Fragment matrix-core kernel (8 < N <= 64, packed model; fp32, or bf16
+// inputs widened exactly to fp32: a bf16 model's image carries this fp32
+// fragment section, and X and C are widened as they are staged). The packed
 // model holds, per 16-column block, the 16x16x4 A operands in the order the
 // waves consume them (see pack_frag_kernel): compute wave w's lane
 // l = (d, q), d = l % 16, q = l / 16, covers the MS consecutive rows
@@ -38,9 +40,19 @@ struct FragBuf {
   float4 a[MS / 4];
 };
 
-template <int NTI, int MS>
+// Four consecutive elements starting at element 4*i (16-byte or 8-byte aligned), as fp32.
+__device__ __forceinline__ float4 load4w(const float* p, int64_t i) {
+  return reinterpret_cast<const float4*>(p)[i];
+}
+__device__ __forceinline__ float4 load4w(const bf16raw* p, int64_t i) {
+  const uint2 u = reinterpret_cast<const uint2*>(p)[i];
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+
+template <typename T, int NTI, int MS>
 __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
-    const float* __restrict__ X, const float4* __restrict__ Bf, const float* __restrict__ C,
+    const T* __restrict__ X, const float4* __restrict__ Bf, const T* __restrict__ C,
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
     int nblocks, int cslots, int lds_floats, void* __restrict__ workspace) {
   constexpr int NB = 16 * NTI;
@@ -88,7 +100,6 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     // run of 16*MS floats.
     const int n4 = nb * F / 4;
     const int rot = (int)(((int64_t)blockIdx.x * 37 * 64) % n4);
-    const float4* x4 = reinterpret_cast<const float4*>(X);
     float4* xs4 = reinterpret_cast<float4*>(xs);
     const int spare4 = (NB * F + 16 * MS + 3) / 4;
     constexpr int kXB = NTI * MS / 4 < 40 ? NTI * MS / 4 : 40;
@@ -100,19 +111,18 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
         const int i = base + j * kThreads + tid;
         const int r = i + rot >= n4 ? i + rot - n4 : i + rot;
         at[j] = i < n4 ? r : spare4;
-        v[j] = x4[i < n4 ? r : rot];
+        v[j] = load4w(X, i < n4 ? r : rot);
       }
 #pragma unroll
       for (int j = 0; j < kXB; ++j) xs4[at[j]] = v[j];
     }
-    for (int e = 4 * n4 + tid; e < nb * F; e += kThreads) xs[e] = X[e];
+    for (int e = 4 * n4 + tid; e < nb * F; e += kThreads) xs[e] = load_elem(X, e);
     for (int e = tid; e < 16 * MS; e += kThreads) xs[nb * F + e] = 0.0f;
     // block i's K*16 C values are one contiguous run of the column tiles
     const int kc4 = K * kW / 4;
     for (int e = tid; e < nmine * kc4; e += kThreads) {
       const int b = e / kc4, r = e - b * kc4;
-      reinterpret_cast<float4*>(cs)[e] =
-          reinterpret_cast<const float4*>(C + (int64_t)walk.block_of(b) * K * kW)[r];
+      reinterpret_cast<float4*>(cs)[e] = load4w(C + (int64_t)walk.block_of(b) * K * kW, r);
     }
   }
   __syncthreads();
@@ -250,8 +260,10 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
 }
 
 // Writes the fragment section: out[((blk*4 + w)*(MS/4) + g)*64 + l][e] =
-// B[4*MS*w + MS*(l/16) + 4g + e][16 blk + l%16], zero past F or D.
-__global__ __launch_bounds__(256) void pack_frag_kernel(const float* __restrict__ B,
+// B[4*MS*w + MS*(l/16) + 4g + e][16 blk + l%16], zero past F or D (fp32; a
+// bf16 B widened exactly).
+template <typename T>
+__global__ __launch_bounds__(256) void pack_frag_kernel(const T* __restrict__ B,
                                                         float* __restrict__ out, int64_t F,
                                                         int64_t D, int64_t nblk, int MS) {
   const int64_t per_blk = (int64_t)256 * MS;  // 16 columns x 16*MS rows
@@ -262,54 +274,60 @@ __global__ __launch_bounds__(256) void pack_frag_kernel(const float* __restrict_
                   w = (i / (64 * MS)) % 4, blk = i / per_blk;
     const int64_t f = 4 * MS * w + MS * (l / 16) + 4 * g + e;
     const int64_t col = blk * kW + l % 16;
-    out[i] = (f < F && col < D) ? B[f * D + col] : 0.0f;
+    out[i] = (f < F && col < D) ? load_elem(B, f * D + col) : 0.0f;
   }
 }
 
 
-template <int NTI, int MS>
+template <typename T, int NTI, int MS>
 hipError_t launch_frag(const SmallPlan& p, const Args& a, const void* frag) {
-  const hipError_t attr = allow_lds<&small_frag_mfma_kernel<NTI, MS>>();
+  const hipError_t attr = allow_lds<&small_frag_mfma_kernel<T, NTI, MS>>();
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((small_frag_mfma_kernel<NTI, MS>), dim3(p.grid), dim3(kFragThreads), p.lds,
-                     a.stream, (const float*)a.X, (const float4*)frag, (const float*)a.C,
+  hipLaunchKernelGGL((small_frag_mfma_kernel<T, NTI, MS>), dim3(p.grid), dim3(kFragThreads), p.lds,
+                     a.stream, (const T*)a.X, (const float4*)frag, (const T*)a.C,
                      a.labels, a.scores, a.N, a.F, a.D, a.K, a.act, p.nblocks, p.cslots,
                      (int)(p.lds / sizeof(float)), a.ws);
   return hipGetLastError();
 }
 
-template <int NTI>
+template <typename T, int NTI>
 hipError_t launch_frag_ms(const SmallPlan& p, const Args& a, const void* frag) {
   switch (p.ms) {
-    case 12: return launch_frag<NTI, 12>(p, a, frag);
-    case 24: return launch_frag<NTI, 24>(p, a, frag);
-    case 36: return launch_frag<NTI, 36>(p, a, frag);
-    case 48: return launch_frag<NTI, 48>(p, a, frag);
-    default: return launch_frag<NTI, 64>(p, a, frag);
+    case 12: return launch_frag<T, NTI, 12>(p, a, frag);
+    case 24: return launch_frag<T, NTI, 24>(p, a, frag);
+    case 36: return launch_frag<T, NTI, 36>(p, a, frag);
+    case 48: return launch_frag<T, NTI, 48>(p, a, frag);
+    default: return launch_frag<T, NTI, 64>(p, a, frag);
   }
 }
 
+template <typename T>
 hipError_t launch_frag_nti(const SmallPlan& p, const Args& a, const void* frag) {
   switch (p.nb) {
-    case 1: return launch_frag_ms<1>(p, a, frag);
-    case 2: return launch_frag_ms<2>(p, a, frag);
-    case 3: return launch_frag_ms<3>(p, a, frag);
-    default: return launch_frag_ms<4>(p, a, frag);
+    case 1: return launch_frag_ms<T, 1>(p, a, frag);
+    case 2: return launch_frag_ms<T, 2>(p, a, frag);
+    case 3: return launch_frag_ms<T, 3>(p, a, frag);
+    default: return launch_frag_ms<T, 4>(p, a, frag);
   }
 }
 
 }  // namespace
 
-hipError_t launch_frag_family(SmallPlan& p, const Args& a, const void* frag) {
+hipError_t launch_frag_family(SmallPlan& p, const Args& a, const void* frag, int dt) {
   widen_for_final(p, a.N, a.K);
-  return launch_frag_nti(p, a, frag);
+  return dt == 0 ? launch_frag_nti<float>(p, a, frag) : launch_frag_nti<bf16raw>(p, a, frag);
 }
 
 hipError_t launch_pack_frag(const void* B, void* out, int64_t F, int64_t D, int64_t nblk, int ms,
-                            hipStream_t stream) {
+                            int dt, hipStream_t stream) {
   const int64_t g = cdiv(nblk * 256 * ms, 256);
-  hipLaunchKernelGGL(pack_frag_kernel, dim3((unsigned)(g < 65536 ? g : 65536)), dim3(256), 0,
-                     stream, (const float*)B, static_cast<float*>(out), F, D, nblk, ms);
+  const dim3 grid((unsigned)(g < 65536 ? g : 65536));
+  if (dt == 0)
+    hipLaunchKernelGGL(pack_frag_kernel<float>, grid, dim3(256), 0, stream, (const float*)B,
+                       static_cast<float*>(out), F, D, nblk, ms);
+  else
+    hipLaunchKernelGGL(pack_frag_kernel<bf16raw>, grid, dim3(256), 0, stream,
+                       (const bf16raw*)B, static_cast<float*>(out), F, D, nblk, ms);
   return hipGetLastError();
 }
 

@@ -34,6 +34,7 @@ CASES = [
     (32, 561, 10240, 6, "f32", True, "small_frag_mfma_kernel"),
     (64, 617, 10240, 26, "f32", True, "small_valu_kernel"),
     (200, 561, 10240, 6, "f32", True, "small_mfma_kernel"),
+    (32, 561, 10240, 6, "bf16", True, "small_frag_mfma_kernel"),
     (16, 617, 4096, 26, "bf16", True, "large_fused_kernel"),
     (16, 3072, 1000, 5, "bf16", False, "large_chunked_dma_kernel"),
 ]
@@ -67,7 +68,7 @@ def test_deterministic_repeats_bit_identical(hd, N, F, D, K, dtype, packed, kern
     assert rep["ok"], rep
 
 
-@pytest.mark.parametrize("N,F,D,K,dtype,packed,kernel", CASES[:8])
+@pytest.mark.parametrize("N,F,D,K,dtype,packed,kernel", CASES[:9])
 def test_deterministic_integer_bit_exact(hd, N, F, D, K, dtype, packed, kernel):
     """Small integers: every sum is exact in any order, so the fixed-order
     reduction must reproduce the oracle bit for bit."""

@@ -220,7 +220,10 @@ INTEGER = [
     (300, 617, 4096, 26, "f32", False, "large_fused_kernel"),
     (300, 617, 4096, 26, "bf16", True, "large_fused_kernel"),
     (257, 31, 700, 3, "bf16", False, "large_fused_kernel"),
-    (32, 561, 2048, 6, "bf16", True, "large_fused_kernel"),
+    (32, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),
+    (16, 561, 10240, 6, "bf16", True, "small_frag_mfma_kernel"),
+    (40, 301, 1000, 16, "bf16", True, "small_frag_mfma_kernel"),
+    (32, 561, 2048, 17, "bf16", True, "large_fused_kernel"),
     (4, 561, 2048, 6, "bf16", True, "small_flat_kernel"),
     (200, 3072, 1024, 10, "bf16", True, "large_chunked_dma_kernel"),
     (130, 2600, 512, 100, "bf16", False, "large_chunked_dma_kernel"),
@@ -254,6 +257,7 @@ TIES = [
     (32, 40, 512, "f32", True, "small_frag_mfma_kernel"),
     (64, 200, 1024, "f32", True, "small_frag_mfma_kernel"),
     (100, 2560, 512, "bf16", True, "large_chunked_dma_kernel"),
+    (32, 40, 512, "bf16", True, "small_frag_mfma_kernel"),
     (100, 2560, 512, "f32", True, "large_chunked_kernel"),
     (100, 2561, 512, "bf16", False, "large_chunked_kernel"),
 ]
@@ -397,13 +401,14 @@ def test_packed_model_matches_raw(hd, N, dtype):
 # f-chunks), the fragment matrix-core kernel (fp32, N > 8: one to four sample
 # tiles, every rows-per-lane size, rows that wrap inside a float4 of X), the
 # persistent matrix-core kernel where the fragment kernel's LDS does not fit,
-# and the VALU kernel (bf16, N > 8).
+# and the fragment kernel on bf16 models (fp32 fragments, X and C widened).
 PACKED_SMALL = [(1, 561, 10240, 6, "f32"), (3, 20, 1000, 4, "f32"), (8, 1100, 777, 9, "f32"),
                 (7, 300, 2050, 3, "bf16"), (9, 64, 1000, 5, "f32"), (32, 561, 10240, 6, "f32"),
                 (64, 561, 4096, 6, "f32"), (40, 130, 3000, 100, "f32"), (20, 90, 1000, 7, "bf16"),
                 (64, 1500, 513, 3, "bf16"), (17, 900, 333, 2, "f32"), (64, 200, 1000, 3, "f32"),
                 (12, 5, 64, 3, "f32"), (16, 4, 100, 2, "f32"), (48, 700, 2000, 26, "f32"),
-                (24, 300, 1000, 16, "f32"), (10, 100, 500, 13, "f32")]
+                (24, 300, 1000, 16, "f32"), (10, 100, 500, 13, "f32"),
+                (32, 561, 10240, 6, "bf16"), (16, 1023, 999, 16, "bf16"), (9, 5, 64, 2, "bf16")]
 
 
 @pytest.mark.parametrize("N,F,D,K,dtype", PACKED_SMALL)
