@@ -173,7 +173,8 @@ def run_train(args, w):
     value = w.N / (ms / 1e3)
     flops = 2.0 * w.N * w.F * w.D
     roof = {"bound": "mfma", "achieved": flops / (ms / 1e3) / 1e12,
-            "peak": MFMA_PEAK_TFLOPS[dtype], "unit": PEAK_UNIT[dtype], "traffic": None,
+            "peak": MFMA_PEAK_TFLOPS[dtype], "unit": PEAK_UNIT[dtype],
+            "traffic": recorded_traffic(w.name + "_train", kernel, dtype),
             "kernel_time": "whole step (fill + class sums + HardSign)"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()}
@@ -188,6 +189,7 @@ def run_train(args, w):
                    "model": "B tiled once before timing"},
         "roofline": roof,
     }
+    calib_copies(args, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_train(w, X, B, y, args.cpu_seconds)
     print(json.dumps(out), flush=True)
@@ -255,7 +257,8 @@ def run_stream(args, w):
     flops = 2.0 * w.N * w.D * (w.F + w.K)
     hbm_per_launch = 4 * (w.F * w.D + w.K * w.D + nbatch * w.N * w.F) + 4 * nbatch * w.N
     roof = {"bound": "mfma", "achieved": flops / s_per_batch / 1e12,
-            "peak": MFMA_PEAK_TFLOPS["f32"], "unit": "TFLOP/s", "traffic": None}
+            "peak": MFMA_PEAK_TFLOPS["f32"], "unit": "TFLOP/s",
+            "traffic": recorded_traffic(f"{w.name}_stream{nbatch}", "stream_frag_kernel", "f32")}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["hbm_GBs"] = hbm_per_launch / (ms / 1e3 / steps) / 1e9
     roof = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()}
@@ -271,6 +274,7 @@ def run_stream(args, w):
                    "kernel": "stream_frag_kernel", "model": "packed once before timing"},
         "roofline": roof,
     }
+    calib_copies(args, dev)
     print(json.dumps(out), flush=True)
 
 
@@ -366,7 +370,7 @@ def run(args, w):
     # Roofline of the dominant (only) kernel of a step: one launch per step.
     launch_s = ms_per_step / 1e3
     kernel = hd.infer_kernel(w.N, w.F, w.D, w.K, Xd.dtype, packed=True)
-    traffic = recorded_traffic(w.name, kernel)
+    traffic = recorded_traffic(w.name, kernel, dtype)
     if small:
         alg_bytes = alg_bytes_of(w, dtype)
         roof = {"bound": "hbm", "achieved": alg_bytes / launch_s / 1e9, "peak": HBM_PEAK_GBS,
@@ -398,16 +402,24 @@ def run(args, w):
         if small and fl.get("stream_read_GBs"):
             roof["measured_peak"] = fl["stream_read_GBs"]
             roof["frac_of_measured"] = round(roof["achieved"] / fl["stream_read_GBs"], 4)
-    if args.calib_copy_mib > 0:
-        n = args.calib_copy_mib << 18  # fp32 elements
-        src = torch.ones(n, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
+    calib_copies(args, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, X, B, C, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def calib_copies(args, dev):
+    """Three plain device-to-device copies of --calib-copy-mib MiB after the
+    timed work: the reference dispatches for scaling hardware byte counters."""
+    if args.calib_copy_mib <= 0:
+        return
+    import torch
+    n = args.calib_copy_mib << 18  # fp32 elements
+    src = torch.ones(n, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
 
 
 def alg_bytes_of(w, dtype) -> int:
@@ -495,10 +507,10 @@ def source_digest() -> str:
     return h.hexdigest()
 
 
-def recorded_traffic(workload: str, kernel: str):
+def recorded_traffic(workload: str, kernel: str, dtype: str):
     """HBM bytes per launch from the committed counter summaries under
     profiles/ (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy's readings),
-    or None when none matches this workload, kernel and source digest."""
+    or None when none matches this workload, kernel, dtype and source digest."""
     if not os.path.isdir(PROFILES):
         return None
     digest = source_digest()
@@ -511,7 +523,7 @@ def recorded_traffic(workload: str, kernel: str):
                     continue
                 kv = dict(t.split("=", 1) for t in line.split()[1:] if "=" in t)
                 if (kv.get("workload") == workload and kv.get("kernel") == kernel
-                        and kv.get("source_sha256") == digest):
+                        and kv.get("dtype") == dtype and kv.get("source_sha256") == digest):
                     return int(kv["bytes_per_launch"])
     return None
 
