@@ -209,8 +209,9 @@ hd_status hd_infer_stream(const void *X, const void *packed, const uint32_t *rea
  * scratch its kernels need (tickets, replicated partial scores, split-D
  * partials) is a fixed device array of hd_noalloc_scratch_bytes() bytes
  * (4 MiB) inside the library, one per GPU, held until the process ends.
- * Calls whose scratch need (hd_infer_packed_workspace_bytes) exceeds that
- * return HD_ERR_WORKSPACE before anything is enqueued. Each call first
+ * Calls whose scratch need in their mode (default or HD_DETERMINISTIC; at
+ * most hd_infer_packed_workspace_bytes) exceeds that return HD_ERR_WORKSPACE
+ * before anything is enqueued. Each call first
  * clears the part it uses (a fill kernel on `stream`), so the array's
  * contents from an earlier call do not matter. All calls on one GPU share
  * the array: calls that overlap in time on one GPU (other streams, other

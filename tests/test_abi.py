@@ -219,3 +219,23 @@ def test_deterministic_flag(L):
     assert L.hd_infer_stream(FAKE, FAKE, None, FAKE, None, None, 1, 4, 8, 64, 3, 0, DET, FAKE,
                              1 << 20, None) == hd.HD_ERR_UNSUPPORTED
     assert L.hd_encode(FAKE, FAKE, FAKE, 4, 8, 16, 0, DET, None) == hd.HD_ERR_ARG
+
+
+def test_routes_of_new_paths(L):
+    """Kernel choice of the bf16 fragment route, the training kernels and the
+    int8 variant (host planning only)."""
+    k = L.hd_infer_kernel
+    # packed bf16 small batches: the fragment kernel (fp32 fragments); raw: large-batch
+    assert k(32, 561, 10240, 6, hd.HD_BF16, 1) == b"small_frag_mfma_kernel"
+    assert k(32, 561, 10240, 6, hd.HD_BF16, 0) == b"large_fused_kernel"
+    assert k(32, 561, 10240, 17, hd.HD_BF16, 1) == b"large_fused_kernel"  # K > 16
+    b = L.hd_bundle_kernel
+    assert b(16384, 3072, 10240, 10, hd.HD_BF16, 1) == b"bundle_dma_kernel"
+    assert b(16384, 3072, 10240, 10, hd.HD_I8, 1) == b"bundle_dma_kernel"
+    assert b(16384, 3071, 10240, 10, hd.HD_BF16, 1) == b"bundle_mfma_kernel"  # F % 8 != 0
+    assert b(4096, 784, 10240, 10, hd.HD_F32, 1) == b"bundle_mfma_kernel"
+    assert b(4096, 784, 10240, 129, hd.HD_F32, 1) == b""      # packed path: K <= 128
+    assert b(4096, 784, 10240, 512, hd.HD_F32, 0) == b"bundle_valu_kernel"
+    assert b(4096, 784, 10240, 513, hd.HD_F32, 0) == b""
+    # the packed image of a bf16 model carries an fp32 fragment section
+    assert L.hd_model_packed_bytes(561, 10240, 6, hd.HD_BF16) >= 576 * 10240 * 4
