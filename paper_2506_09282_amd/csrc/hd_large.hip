@@ -990,8 +990,8 @@ __device__ __forceinline__ void lds_reads_complete(uint4 (&v)[NT]) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16 F-chunked variant with the X chunks double-buffered in LDS and filled
-// by direct buffer-to-LDS loads (lane l of a 16-byte load lands at the wave's
+// bf16 / int8 F-chunked variant with the X chunks double-buffered in LDS and
+// filled by direct buffer-to-LDS loads (lane l of a 16-byte load lands at the wave's
 // LDS base + 16 l; out-of-range offsets deliver zeros). The loads of the next
 // chunk are issued two per f-step at the start of the current one, so they
 // overlap the matrix instructions. Chunks are a fixed kDmaFsc f-steps (the
@@ -1000,7 +1000,7 @@ __device__ __forceinline__ void lds_reads_complete(uint4 (&v)[NT]) {
 // publishes a chunk wait only for the LDS loads, not for the ring behind them.
 // An LDS row is W = 2 kDmaFsc + 1 slots of 16 bytes: two per f-step plus one
 // padding slot that keeps the 32 rows of a fragment read on distinct banks.
-// Requires F % 8 == 0 and a 16-byte aligned X.
+// Requires F to be a whole number of 16-byte groups and a 16-byte aligned X.
 // ---------------------------------------------------------------------------
 constexpr int kDmaFsc = 16;
 
@@ -1017,23 +1017,26 @@ __host__ __device__ constexpr int dma_loads_per_wave(int ntiles) {
   return (32 * ntiles * (2 * kDmaFsc + 1) + kThreads - 1) / kThreads;
 }
 
-template <int NTILES, int KB, int ACT>
+template <class Tr, int NTILES, int KB, int ACT>
 __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
-    const bf16raw* __restrict__ X, const uint4* __restrict__ Bp, const uint4* __restrict__ Cp,
-    int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int K, int ndb,
-    int DS, void* __restrict__ workspace) {
-  typedef TrBF16 Tr;
+    const typename Tr::elem* __restrict__ X, const uint4* __restrict__ Bp,
+    const uint4* __restrict__ Cp, int32_t* __restrict__ labels, float* __restrict__ scores, int N,
+    int F, int K, int ndb, int DS, void* __restrict__ workspace) {
+  typedef typename Tr::elem T;
+  static_assert(Tr::kEsz <= 2, "16-byte slots of bf16 or int8");
   constexpr int NT = 32 * NTILES;
   constexpr int UPW = dma_units_per_wave(NTILES, KB);  // units per wave per X pass
   constexpr int kPF = UPW > 1 ? 4 : prefetch_of(NTILES, KB);
   constexpr int FSC = kDmaFsc;
   constexpr int W = 2 * FSC + 1;                 // slots per LDS row
-  constexpr int pitch = 8 * W;                   // elements
+  constexpr int pitch = Tr::kVec * W;            // elements
   constexpr int P = dma_loads_per_wave(NTILES);  // LDS loads per wave per chunk
   constexpr int kDmaSteps = (P + 1) / 2;         // the first steps issue them, two each
   constexpr int kAfter = 2 * UPW * (FSC - kDmaSteps);  // ring loads issued after the last one
   constexpr int kWait = kAfter < 2 * UPW * kPF ? kAfter : 2 * UPW * kPF;
-  constexpr int buf_elems = P * kThreads * 8;
+  constexpr int buf_elems = P * kThreads * Tr::kVec;
+  constexpr int kTileBytes = 32 * pitch * Tr::kEsz;  // 32 rows of a buffer
+  constexpr int kStepBytes = Tr::kFStep * Tr::kEsz;  // one f-step of a row
   static_assert(FSC % kPF == 0 && kDmaSteps <= FSC && kWait <= 63, "chunk schedule");
   // s_waitcnt immediate: vmcnt(kWait), expcnt and lgkmcnt not waited on
   constexpr int kWaitImm = 0x0F70 | (kWait & 15) | ((kWait >> 4) << 14);
@@ -1053,13 +1056,13 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
   const int u_begin = (int)((int64_t)units * slice / DS);
   const int u_end = (int)((int64_t)units * (slice + 1) / DS);
 
-  bf16raw* xb = reinterpret_cast<bf16raw*>(lds);  // two buffers of buf_elems
-  const bf16raw* xzero = xb + 2 * buf_elems;      // 16-byte zero slot
+  T* xb = reinterpret_cast<T*>(lds);        // two buffers of buf_elems
+  const T* xzero = xb + 2 * buf_elems;      // 16-byte zero slot
   if (tid == 0) *reinterpret_cast<uint4*>(xb + 2 * buf_elems) = make_uint4(0u, 0u, 0u, 0u);
 
   // The tile's rows of X as one buffer resource; rows past N are out of range.
   const __amdgpu_buffer_rsrc_t xrsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<bf16raw*>(X + (int64_t)n0 * F), 0, rows * F * 2, 0x00020000);
+      const_cast<T*>(X + (int64_t)n0 * F), 0, rows * F * Tr::kEsz, 0x00020000);
   // Load p of this wave for chunk ch into buffer `buf`: slot q of the buffer.
   auto dma = [&](int ch, int p, int buf) {
     int q = (p * kWaves + wave) * 64 + lane;
@@ -1067,13 +1070,13 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
     // the chunk loop would hold dozens of registers for the whole unit
     asm volatile("" : "+v"(q));
     const int r = q / W, rem = q - r * W;
-    const int col = (ch * FSC + (rem >> 1)) * 16 + (rem & 1) * 8;
+    const int col = (ch * FSC + (rem >> 1)) * Tr::kFStep + (rem & 1) * Tr::kVec;
     const bool ok = r < rows && rem < 2 * FSC && col < F;
-    const unsigned off = ok ? (unsigned)((r * F + col) * 2) : 0x80000000u;
+    const unsigned off = ok ? (unsigned)((r * F + col) * Tr::kEsz) : 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         xrsrc,
         (__attribute__((address_space(3))) void*)(xb + buf * buf_elems +
-                                                  (p * kWaves + wave) * 64 * 8),
+                                                  (p * kWaves + wave) * 64 * Tr::kVec),
         16, off, 0, 0, 0);
   };
 
@@ -1145,7 +1148,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
       const int nbuf = cur ^ 1;
       uint4 xfr[2][NTILES];
 #pragma unroll
-      for (int t = 0; t < NTILES; ++t) xfr[0][t] = lds_read16_issue(xc + t * 64 * pitch);
+      for (int t = 0; t < NTILES; ++t) xfr[0][t] = lds_read16_issue(xc + t * kTileBytes);
 #pragma unroll
       for (int s = 0; s < FSC; ++s) {
         const int i = s % kPF;
@@ -1153,7 +1156,7 @@ __global__ __launch_bounds__(kThreads, 1) void large_chunked_dma_kernel(
 #pragma unroll
         for (int t = 0; t < NTILES; ++t)
           xfr[(s + 1) & 1][t] =
-              lds_read16_issue(s + 1 < fsn ? xc + t * 64 * pitch + (s + 1) * 32 : xz);
+              lds_read16_issue(s + 1 < fsn ? xc + t * kTileBytes + (s + 1) * kStepBytes : xz);
 #pragma unroll
         for (int j = 0; j < UPW; ++j)
 #pragma unroll
@@ -1677,6 +1680,24 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) 
       break;
     }
   }
+  // The double-buffered kernel: 64-sample tiles, X chunks by buffer-to-LDS
+  // loads (16-byte groups of bf16 or int8).
+  auto try_dma = [&]() {
+    if (!(Tr::kEsz <= 2 && F % Tr::kVec == 0 && x16)) return false;
+    // two buffers of P * kThreads slots of 16 bytes, plus the zero slot
+    const int dnt = kDmaNtiles;
+    const size_t drbytes = (size_t)kWaves * 32 * dnt * 32 * kbr * 4;
+    const size_t dbytes = (size_t)2 * dma_loads_per_wave(dnt) * kThreads * 16 + 16;
+    if (dbytes > (size_t)kLdsBytes || drbytes > (size_t)kLdsBytes) return false;
+    c.dma = true;
+    c.ntiles_per_wg = dnt;
+    c.fsc = kDmaFsc;
+    c.lds = dbytes > drbytes ? dbytes : drbytes;
+    return true;
+  };
+  // int8 rows are short enough that a wide F still fits LDS as a 32-sample
+  // tile; the double-buffered kernel uses each B fragment for 64 samples.
+  if (Tr::kEsz == 1 && c.ntiles_per_wg == 1) try_dma();
   if (!c.ntiles_per_wg) {
     // X tile too large for LDS: stream it in chunks of f-steps
     const int nt = chunk_ntiles<Tr>(kbr);
@@ -1689,18 +1710,7 @@ LargeCfg large_cfg(int64_t N, int64_t F, int64_t D, int64_t K, bool x16 = true) 
     c.fsc = fsc;
     const size_t xbytes = (size_t)32 * nt * (fsc * Tr::kFStep + pad) * Tr::kEsz + 16;
     c.lds = xbytes > rbytes ? xbytes : rbytes;
-    if (Tr::kEsz == 2 && F % 8 == 0 && x16) {
-      // two buffers of P * kThreads slots of 16 bytes, plus the zero slot
-      const int dnt = kDmaNtiles;
-      const size_t drbytes = (size_t)kWaves * 32 * dnt * 32 * kbr * 4;
-      const size_t dbytes = (size_t)2 * dma_loads_per_wave(dnt) * kThreads * 16 + 16;
-      if (dbytes <= (size_t)kLdsBytes && drbytes <= (size_t)kLdsBytes) {
-        c.dma = true;
-        c.ntiles_per_wg = dnt;
-        c.fsc = kDmaFsc;
-        c.lds = dbytes > drbytes ? dbytes : drbytes;
-      }
-    }
+    try_dma();
   }
   c.kb = kbr;
   c.ntiles = cdiv(N, 32 * c.ntiles_per_wg);
@@ -1734,12 +1744,13 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
   const dim3 grid((unsigned)(c.ntiles * c.ds)), block(kThreads);
   if (c.fsc > 0) {
     if (c.dma) {
-      if constexpr (Tr::kEsz == 2 && NTILES == kDmaNtiles) {
-        const hipError_t dattr = allow_large_lds<&large_chunked_dma_kernel<NTILES, KB, ACT>>();
+      if constexpr (Tr::kEsz <= 2 && NTILES == kDmaNtiles) {
+        const hipError_t dattr =
+            allow_large_lds<&large_chunked_dma_kernel<Tr, NTILES, KB, ACT>>();
         if (dattr != hipSuccess) return dattr;
-        hipLaunchKernelGGL((large_chunked_dma_kernel<NTILES, KB, ACT>), grid, block, c.lds,
-                           stream, (const bf16raw*)X, Bp, Cp, labels, scores, (int)N, (int)F,
-                           (int)K, ndb, c.ds, ws);
+        hipLaunchKernelGGL((large_chunked_dma_kernel<Tr, NTILES, KB, ACT>), grid, block, c.lds,
+                           stream, (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N,
+                           (int)F, (int)K, ndb, c.ds, ws);
         return hipGetLastError();
       }
       return hipErrorInvalidValue;

@@ -45,18 +45,21 @@ def check(y, S, ref):
 
 
 # (N, F, D, K, packed, kernel): X tile resident (one, two and four 32-sample
-# tiles per workgroup, one to four class blocks), X streamed in F-chunks (F
-# divisible by 16 and ragged), one sample (split of D), ragged D.
+# tiles per workgroup, one to four class blocks), X streamed in F-chunks
+# (double-buffered by buffer-to-LDS loads when F is a multiple of 16, through
+# registers when ragged), one sample (split of D), ragged D.
 CASES = [
     (300, 617, 4096, 26, True, "large_fused_kernel"),
     (300, 617, 4096, 26, False, "large_fused_kernel"),
     (1, 561, 10240, 6, True, "large_fused_kernel"),
     (129, 300, 2000, 100, True, "large_fused_kernel"),
     (77, 1000, 999, 40, False, "large_fused_kernel"),
-    (200, 3072, 1024, 10, True, "large_fused_kernel"),
-    (200, 6016, 1024, 10, True, "large_chunked_kernel"),
+    (200, 3001, 1024, 10, True, "large_fused_kernel"),
+    (200, 3072, 1024, 10, True, "large_chunked_dma_kernel"),
+    (1000, 4096, 2048, 20, True, "large_chunked_dma_kernel"),
+    (200, 6016, 1024, 10, True, "large_chunked_dma_kernel"),
+    (33, 8192, 512, 128, False, "large_chunked_dma_kernel"),
     (130, 6001, 700, 70, True, "large_chunked_kernel"),
-    (33, 8192, 512, 128, False, "large_chunked_kernel"),
 ]
 
 
@@ -71,7 +74,8 @@ def test_int8_bit_exact(hd, N, F, D, K, packed, kernel):
 
 
 @pytest.mark.parametrize("N,F,kernel", [(300, 40, "large_fused_kernel"),
-                                        (100, 6000, "large_chunked_kernel")])
+                                        (100, 6000, "large_chunked_dma_kernel"),
+                                        (100, 6001, "large_chunked_kernel")])
 def test_int8_zero_sums_and_argmax_ties(hd, N, F, kernel):
     """X, B in {-1, 0, 1}: many encoding sums are exactly 0 (HardSign +1);
     duplicated class rows tie, and the lowest index must win."""
