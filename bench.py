@@ -52,6 +52,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=None)
     p.add_argument("--workload", default="activity_n32", choices=sorted(hd_inputs.WORKLOADS))
     p.add_argument("--dtype", default=None, choices=["f32", "bf16", "i8"])
+    p.add_argument("--raw", action="store_true",
+                   help="time hd_infer on B and C as given (no packed model): the large-batch "
+                        "route re-tiles B and C into the workspace inside every call")
     p.add_argument("--train", action="store_true",
                    help="single-pass training: one step = clear the class counts, "
                         "hd_bundle_classes_packed over the workload's N labelled samples, "
@@ -306,19 +309,25 @@ def run(args, w):
         Bs.append(Bs[0].clone())
         Cs.append(Cs[0].clone())
     # the model is packed once, outside the timed region, like weights loaded
-    # for serving; every step reads the packed image
-    models = [hd.pack_model(b, c) for b, c in zip(Bs, Cs)]
-    del Bs, Cs
+    # for serving; every step reads the packed image (with --raw, B and C as
+    # given, and every call packs what it needs itself)
+    models = None if args.raw else [hd.pack_model(b, c) for b, c in zip(Bs, Cs)]
+    if not args.raw:
+        del Bs, Cs
     labels = torch.empty(w.N, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 
     stream = torch.cuda.Stream(device=dev)
-    ws_bytes = int(hd.lib().hd_infer_packed_workspace_bytes(
-        w.N, w.F, w.D, w.K, {"f32": hd.HD_F32, "bf16": hd.HD_BF16, "i8": hd.HD_I8}[dtype]))
+    hdt = {"f32": hd.HD_F32, "bf16": hd.HD_BF16, "i8": hd.HD_I8}[dtype]
+    ws_bytes = int(hd.lib().hd_infer_workspace_bytes(w.N, w.F, w.D, w.K, hdt) if args.raw
+                   else hd.lib().hd_infer_packed_workspace_bytes(w.N, w.F, w.D, w.K, hdt))
     ws = torch.zeros(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
 
     def step(i):
-        hd.infer_packed(Xd, models[i % copies], out=(labels, None), workspace=ws)
+        if args.raw:
+            hd.infer(Xd, Bs[i % copies], Cs[i % copies], out=(labels, None), workspace=ws)
+        else:
+            hd.infer_packed(Xd, models[i % copies], out=(labels, None), workspace=ws)
 
     with torch.cuda.stream(stream):
         for i in range(3):
@@ -369,8 +378,8 @@ def run(args, w):
 
     # Roofline of the dominant (only) kernel of a step: one launch per step.
     launch_s = ms_per_step / 1e3
-    kernel = hd.infer_kernel(w.N, w.F, w.D, w.K, Xd.dtype, packed=True)
-    traffic = recorded_traffic(w.name, kernel, dtype)
+    kernel = hd.infer_kernel(w.N, w.F, w.D, w.K, Xd.dtype, packed=not args.raw)
+    traffic = recorded_traffic(w.name + ("_raw" if args.raw else ""), kernel, dtype)
     if small:
         alg_bytes = alg_bytes_of(w, dtype)
         roof = {"bound": "hbm", "achieved": alg_bytes / launch_s / 1e9, "peak": HBM_PEAK_GBS,
@@ -393,7 +402,9 @@ def run(args, w):
                                + ", HardSign, seed 0",
                    "global_batch": w.N, "parallelism": "single GPU",
                    "model_copies_rotated": copies, "timing": "hip graph" if use_graph else "eager",
-                   "kernel": kernel, "model": "packed once before timing"},
+                   "kernel": kernel,
+                   "model": ("B and C as given (hd_infer)" if args.raw
+                             else "packed once before timing")},
         "roofline": roof,
     }
     if not args.no_floors:
