@@ -265,6 +265,8 @@ __global__ __launch_bounds__(kStreamThreads, 1) void stream_frag_kernel(
     if (wave == 1) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): C is in LDS
     if (!have0 && tid == 0) s_stop = 1;
     for (int e = tid; e < 16 * MS; e += 256) xs[nb * F + e] = 0.0f;
+    // queue state of batch 1, read by the loaders at the top of batch 0
+    if (tid == 64) s_next = 1 < nbatch ? batch_state(ready, 1u, false) : -1;
   }
   raw_barrier();
 
@@ -385,15 +387,13 @@ __global__ __launch_bounds__(kStreamThreads, 1) void stream_frag_kernel(
   }
   for (; b < nbatch; ++b) {
     if (*(volatile int*)&s_stop) break;
-    if (wave == 0 && b > 0) publish_issue(b - 1);  // sl holds batch b-1's scores
-    // Is the next batch already in the queue? Then waves 0..3 request its X
-    // now; otherwise wave 1 waits for it at the end of this batch (which is
-    // not held up) and moves it alone.
-    if (tid == 64)
-      s_next = b + 1 < nbatch ? batch_state(ready, (unsigned)(b + 1), false) : -1;
-    raw_barrier();
+    // Was the next batch in the queue at the end of the previous one? Then
+    // waves 0..3 request its X first thing; otherwise wave 1 waits for it at
+    // the end of this batch (which is not held up) and moves it alone.
     const int next0 = *(volatile int*)&s_next;
     if (next0 == 1) x_load(b + 1, tid);
+    if (wave == 0 && b > 0) publish_issue(b - 1);  // sl holds batch b-1's scores
+    raw_barrier();
     raw_barrier();
     if (nmine > 1) {
       finish(0);
@@ -424,6 +424,9 @@ __global__ __launch_bounds__(kStreamThreads, 1) void stream_frag_kernel(
       }
     }
     if (wave == 1 && next0 == -1 && b + 1 < nbatch && lane == 0) s_stop = 1;
+    // queue state of batch b+2, read by the loaders at the top of batch b+1
+    if (tid == 64)
+      s_next = b + 2 < nbatch ? batch_state(ready, (unsigned)(b + 2), false) : -1;
     raw_barrier();  // end of batch b: its scores in sl, X of batch b+1 in LDS
   }
   if (wave == 0 && b > 0) {
