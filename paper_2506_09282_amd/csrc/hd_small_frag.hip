@@ -1,4 +1,6 @@
 // Small-batch matrix-core kernel on the packed fragment layout.
+#include <type_traits>
+
 #include "hd_small.hpp"
 
 namespace hd {
@@ -50,7 +52,7 @@ __device__ __forceinline__ float4 load4w(const bf16raw* p, int64_t i) {
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
 }
 
-template <typename T, int NTI, int MS>
+template <typename T, int NTI, int MS, bool RING>
 __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     const T* __restrict__ X, const float4* __restrict__ Bf, const T* __restrict__ C,
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
@@ -75,22 +77,116 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
   const int npairs = nb * K;
   const int nmine = walk.count();
 
-  // compute waves: B fragments of blocks 0, 1, 2
-  FragBuf<MS> b0, b1, b2;
-  // Blocks past the workgroup's last one are "loaded" from a single
-  // broadcast address (one 16-byte request per wave instruction), so the
-  // load count per step never depends on a branch.
-  auto load_b = [&](FragBuf<MS>& x, int i) {
-    const float4* p = i < nmine
-        ? Bf + ((int64_t)walk.block_of(i) * kWaves + cw) * G4 * kWave + lane : Bf;
-    const int stride = i < nmine ? kWave : 0;
+  // The two roles run separate code paths from the first instruction, with
+  // the same barrier count (nmine + 2), so that the compiler's load-counter
+  // bookkeeping for one role's loads never merges with the other's: each
+  // matrix step then waits only for its own block's B, not for loads issued
+  // after it.
+  if (compute) {
+    // B fragments of blocks 0, 1, 2. Blocks past the workgroup's last one
+    // are "loaded" from a single broadcast address (one 16-byte request per
+    // wave instruction), so the load count per step never depends on a branch.
+    FragBuf<MS> b0, b1, b2;
+    auto load_b = [&](FragBuf<MS>& x, int i) {
+      const float4* p = i < nmine
+          ? Bf + ((int64_t)walk.block_of(i) * kWaves + cw) * G4 * kWave + lane : Bf;
+      const int stride = i < nmine ? kWave : 0;
 #pragma unroll
-    for (int g = 0; g < G4; ++g) x.a[g] = p[g * stride];
-  };
-
-  if (compute) {  // the third block goes out after the barrier
+      for (int g = 0; g < G4; ++g) x.a[g] = p[g * stride];
+    };
     load_b(b0, 0);
-    load_b(b1, 1);
+    load_b(b1, 1);  // the third block goes out after the barrier
+    __syncthreads();  // X and the blocks' C values are in LDS
+
+    // X operands: they do not depend on the block, so when the registers
+    // allow they are read from LDS once into registers (no LDS latency
+    // between matrix instructions)
+    constexpr bool kXReg = 3 * MS + NTI * MS <= 180;
+    const int xoff = (lane & 15) * F + 4 * MS * cw + MS * (lane >> 4);
+    float4 xr[kXReg ? G4 : 1][kXReg ? NTI : 1];
+    if (kXReg) {
+#pragma unroll
+      for (int g = 0; g < (kXReg ? G4 : 1); ++g)
+#pragma unroll
+        for (int t = 0; t < (kXReg ? NTI : 1); ++t) {
+          const float* q = xs + xoff + 16 * t * F + 4 * g;
+          xr[g][t] = make_float4(q[0], q[1], q[2], q[3]);
+        }
+    }
+    load_b(b2, 2);
+    auto multiply = [&](const FragBuf<MS>& x, int i) {
+      // two independent accumulator chains per sample tile (steps 4g, 4g+2
+      // and 4g+1, 4g+3), interleaved over the tiles
+      f32x4 acc[NTI][2];
+#pragma unroll
+      for (int t = 0; t < NTI; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int g = 0; g < G4; ++g) {
+        float4 xg[NTI];
+#pragma unroll
+        for (int t = 0; t < NTI; ++t) {
+          if constexpr (kXReg) {
+            xg[t] = xr[g][t];
+          } else {
+            const float* q = xs + xoff + 16 * t * F + 4 * g;
+            xg[t] = make_float4(q[0], q[1], q[2], q[3]);
+          }
+        }
+#pragma unroll
+        for (int t = 0; t < NTI; ++t)
+          acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].x, xg[t].x, acc[t][0], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < NTI; ++t)
+          acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].y, xg[t].y, acc[t][1], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < NTI; ++t)
+          acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].z, xg[t].z, acc[t][0], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < NTI; ++t)
+          acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].w, xg[t].w, acc[t][1], 0, 0, 0);
+      }
+      // lane l holds V^T[d = 4(l/16) + q][n = l%16], q = 0..3: one 16-byte
+      // store into red[i % 2][cw][t][n][d]
+      float4* r = reinterpret_cast<float4*>(red + ((i & 1) * kWaves + cw) * NTI * 256) +
+                  (lane & 15) * 4 + (lane >> 4);
+#pragma unroll
+      for (int t = 0; t < NTI; ++t)
+        r[t * 64] = make_float4(acc[t][0][0] + acc[t][1][0], acc[t][0][1] + acc[t][1][1],
+                                acc[t][0][2] + acc[t][1][2], acc[t][0][3] + acc[t][1][3]);
+    };
+    // Step i (one barrier each): multiply block i and reload its buffer with
+    // block i+3. B buffers are named per step (no register copies, which
+    // would wait on the loads).
+    if constexpr (!RING) {
+      // At most three blocks per workgroup: straight-line steps, no reloads.
+      // Without a loop the compiler counts the outstanding loads exactly, so
+      // step i waits only for block i (the ring's loop makes it wait for
+      // loads issued after block i as well).
+      multiply(b0, 0);
+      __syncthreads();
+      if (nmine > 1) {
+        multiply(b1, 1);
+        __syncthreads();
+      }
+      if (nmine > 2) {
+        multiply(b2, 2);
+        __syncthreads();
+      }
+    } else {
+      auto stepc = [&](FragBuf<MS>& b, int i) {
+        multiply(b, i);
+        load_b(b, i + 3);
+        __syncthreads();
+      };
+      for (int it = 0; it < nmine; it += 3) {
+        stepc(b0, it);
+        if (it + 1 >= nmine) break;
+        stepc(b1, it + 1);
+        if (it + 2 >= nmine) break;
+        stepc(b2, it + 2);
+      }
+    }
+    __syncthreads();  // the finish waves' last step
   } else {
     // X copied verbatim into LDS (xs[n*F + f]). Each workgroup starts at a
     // different offset so that they do not all read the same L2 lines at
@@ -124,134 +220,106 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
       const int b = e / kc4, r = e - b * kc4;
       reinterpret_cast<float4*>(cs)[e] = load4w(C + (int64_t)walk.block_of(b) * K * kW, r);
     }
-  }
-  __syncthreads();
+    __syncthreads();
 
-  // X operands of the compute waves: they do not depend on the block, so
-  // when the registers allow they are read from LDS once into registers
-  // (no LDS latency between matrix instructions)
-  constexpr bool kXReg = 3 * MS + NTI * MS <= 180;
-  const int xoff = (lane & 15) * F + 4 * MS * cw + MS * (lane >> 4);
-  float4 xr[kXReg ? G4 : 1][kXReg ? NTI : 1];
-  if (compute) {
-    if (kXReg) {
+    // Block i's partial scores (Eq. 1, Eq. 8). The four finish waves, one per
+    // SIMD, share the work: on this chip fp32 VALU instructions do not
+    // overlap the fp32 matrix instructions of their SIMD, so the finish work
+    // adds to the matrix time of whichever SIMDs run it. LPS lanes per sample
+    // n (256 / NB, at least 4), each with CPL = 16 / LPS consecutive columns:
+    // a lane sums the four wave partials of its V values, applies HardSign,
+    // and adds its CPL-term share of every class's inner product to its own
+    // running sum (classes in groups of four under a uniform branch, the
+    // group's C reads issued together; a class past K reads class K-1 and
+    // its sum is never used). The LPS shares are added once, after the last
+    // block. Columns past D need no mask: the packed C is zero there.
+    constexpr int LPS = NB <= 16 ? 16 : NB <= 32 ? 8 : 4;
+    constexpr int CPL = 16 / LPS;
+    const int fn = tid / LPS, fc = (tid % LPS) * CPL;
+    float psum[kFragMaxK];
 #pragma unroll
-      for (int g = 0; g < (kXReg ? G4 : 1); ++g)
+    for (int k = 0; k < kFragMaxK; ++k) psum[k] = 0.0f;
+    auto lds_vec = [](const float* p, float (&v)[CPL]) {
+      if constexpr (CPL == 4) {
+        const float4 t = *reinterpret_cast<const float4*>(p);
+        v[0] = t.x;
+        v[1] = t.y;
+        v[2] = t.z;
+        v[3] = t.w;
+      } else if constexpr (CPL == 2) {
+        const float2 t = *reinterpret_cast<const float2*>(p);
+        v[0] = t.x;
+        v[1] = t.y;
+      } else {
+        v[0] = *p;
+      }
+    };
+    auto finish = [&](int i) {
+      if (fn >= nb) return;  // a sample's lanes drop out together
+      // red[i % 2][w][t][n16][16 d]: sample fn = 16 t + n16 is row fn of wave w's part
+      const float* r = red + (i & 1) * kWaves * NTI * 256 + fn * 16 + fc;
+      float v[CPL];
+      lds_vec(r, v);
 #pragma unroll
-        for (int t = 0; t < (kXReg ? NTI : 1); ++t) {
-          const float* q = xs + xoff + 16 * t * F + 4 * g;
-          xr[g][t] = make_float4(q[0], q[1], q[2], q[3]);
-        }
-    }
-    load_b(b2, 2);
-  }
-  auto multiply = [&](const FragBuf<MS>& x, int i) {
-    // two independent accumulator chains per sample tile (steps 4g, 4g+2
-    // and 4g+1, 4g+3), interleaved over the tiles
-    f32x4 acc[NTI][2];
+      for (int w = 1; w < kWaves; ++w) {
+        float u[CPL];
+        lds_vec(r + w * NTI * 256, u);
 #pragma unroll
-    for (int t = 0; t < NTI; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int g = 0; g < G4; ++g) {
-      float4 xg[NTI];
-#pragma unroll
-      for (int t = 0; t < NTI; ++t) {
-        if constexpr (kXReg) {
-          xg[t] = xr[g][t];
-        } else {
-          const float* q = xs + xoff + 16 * t * F + 4 * g;
-          xg[t] = make_float4(q[0], q[1], q[2], q[3]);
-        }
+        for (int c = 0; c < CPL; ++c) v[c] += u[c];
       }
 #pragma unroll
-      for (int t = 0; t < NTI; ++t)
-        acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].x, xg[t].x, acc[t][0], 0, 0, 0);
+      for (int c = 0; c < CPL; ++c) v[c] = activate(v[c], act);
+      const float* cb = cs + i * K * kW + fc;
 #pragma unroll
-      for (int t = 0; t < NTI; ++t)
-        acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].y, xg[t].y, acc[t][1], 0, 0, 0);
+      for (int kg = 0; kg < kFragMaxK / 4; ++kg) {
+        if (4 * kg < K) {
+          float cv[4][CPL];
 #pragma unroll
-      for (int t = 0; t < NTI; ++t)
-        acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].z, xg[t].z, acc[t][0], 0, 0, 0);
+          for (int j = 0; j < 4; ++j) {
+            const int k = 4 * kg + j;
+            lds_vec(cb + (k < K ? k : K - 1) * kW, cv[j]);
+          }
 #pragma unroll
-      for (int t = 0; t < NTI; ++t)
-        acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].w, xg[t].w, acc[t][1], 0, 0, 0);
-    }
-    // lane l holds V^T[d = 4(l/16) + q][n = l%16], q = 0..3: one 16-byte
-    // store into red[i % 2][cw][t][n][d]
-    float4* r = reinterpret_cast<float4*>(red + ((i & 1) * kWaves + cw) * NTI * 256) +
-                (lane & 15) * 4 + (lane >> 4);
+          for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int t = 0; t < NTI; ++t)
-      r[t * 64] = make_float4(acc[t][0][0] + acc[t][1][0], acc[t][0][1] + acc[t][1][1],
-                              acc[t][0][2] + acc[t][1][2], acc[t][0][3] + acc[t][1][3]);
-  };
-  // Block i's partial scores. Finish thread (n, g), a quad of lanes per
-  // sample n, sums the four wave partials of V[n][4g .. 4g+3], applies
-  // HardSign, and forms its 4-term share of every class's inner product
-  // (K <= kFragMaxK, all C reads issued at once); the quad adds its shares
-  // with DPP and lane g keeps classes k = g mod 4 in registers across blocks.
-  // Columns past D need no mask: the packed C is zero there.
-  const int fn = tid >> 2, fg = tid & 3;
-  float sacc[kFragMaxK / 4];
-#pragma unroll
-  for (int j = 0; j < kFragMaxK / 4; ++j) sacc[j] = 0.0f;
-  auto finish = [&](int i) {
-    if (fn >= nb) return;  // whole quads drop out together
-    const float4* r4 = reinterpret_cast<const float4*>(red + (i & 1) * kWaves * NTI * 256);
-    const float4* c4 = reinterpret_cast<const float4*>(cs + i * K * kW);
-    float4 c[kFragMaxK];
-#pragma unroll
-    for (int k = 0; k < kFragMaxK; ++k) c[k] = c4[(k < K ? k : 0) * 4 + fg];
-    float4 v = r4[fn * 4 + fg];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) {
-      const float4 u = r4[w * NTI * 64 + fn * 4 + fg];
-      v.x += u.x;
-      v.y += u.y;
-      v.z += u.z;
-      v.w += u.w;
-    }
-    const float h0 = activate(v.x, act), h1 = activate(v.y, act), h2 = activate(v.z, act),
-                h3 = activate(v.w, act);
-#pragma unroll
-    for (int k = 0; k < kFragMaxK; ++k) {
-      float d = fmaf(h0, c[k].x, fmaf(h1, c[k].y, fmaf(h2, c[k].z, h3 * c[k].w)));
-      d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                         0, __builtin_bit_cast(int, d), 0xB1, 0xf, 0xf, false));
-      d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                         0, __builtin_bit_cast(int, d), 0x4E, 0xf, 0xf, false));
-      sacc[k >> 2] += (k & 3) == fg ? d : 0.0f;
-    }
-  };
-  // Step i (one barrier each, nmine + 1 steps): compute waves multiply block
-  // i and reload its buffer with block i+3; finish waves finish block i-1.
-  // The two roles run separate loops with the same barrier count, so that
-  // the compiler's load-counter bookkeeping for the B ring never crosses the
-  // other role's code. B buffers are named per step (no register copies,
-  // which would wait on the loads).
-  if (compute) {
-    auto stepc = [&](FragBuf<MS>& b, int i) {
-      multiply(b, i);
-      load_b(b, i + 3);
-      __syncthreads();
+            for (int c = 0; c < CPL; ++c) psum[4 * kg + j] = fmaf(v[c], cv[j][c], psum[4 * kg + j]);
+        }
+      }
     };
-    for (int it = 0; it < nmine; it += 3) {
-      stepc(b0, it);
-      if (it + 1 >= nmine) break;
-      stepc(b1, it + 1);
-      if (it + 2 >= nmine) break;
-      stepc(b2, it + 2);
-    }
-    __syncthreads();  // the finish waves' last step
-  } else {
+    // Step i (one barrier each, nmine + 1 steps): finish block i-1 while the
+    // compute waves multiply block i.
     for (int i = 0; i <= nmine; ++i) {
       if (i > 0) finish(i - 1);
       __syncthreads();
     }
+    // The sample's LPS lanes are consecutive, aligned and drop out together.
+    // DPP sums them without LDS traffic: the two quad swaps leave each quad's
+    // total in its lanes, the half-row mirror (lane l of 8 reads lane 7-l)
+    // adds the other quad of 8, the row mirror (l of 16 reads 15-l) the other
+    // half-row; every lane then holds its sample's total.
+    auto dpp_add = [](float d, auto ctrl) {
+      return d + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                               0, __builtin_bit_cast(int, d), decltype(ctrl)::value,
+                                               0xf, 0xf, false));
+    };
+    using QuadSwap1 = std::integral_constant<int, 0xB1>;  // quad_perm [1,0,3,2]
+    using QuadSwap2 = std::integral_constant<int, 0x4E>;  // quad_perm [2,3,0,1]
+    using HalfMirror = std::integral_constant<int, 0x141>;  // row_half_mirror
+    using RowMirror = std::integral_constant<int, 0x140>;   // row_mirror
     if (fn < nb) {
 #pragma unroll
-      for (int k = 0; k < kFragMaxK; ++k)
-        if (k < K && (k & 3) == fg) sl[fn * K + k] = sacc[k >> 2];
+      for (int kg = 0; kg < kFragMaxK / 4; ++kg) {
+        if (4 * kg < K) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int k = 4 * kg + j;
+            float d = dpp_add(dpp_add(psum[k], QuadSwap1{}), QuadSwap2{});
+            if constexpr (LPS >= 8) d = dpp_add(d, HalfMirror{});
+            if constexpr (LPS >= 16) d = dpp_add(d, RowMirror{});
+            if (k < K && tid % LPS == k % LPS) sl[fn * K + k] = d;
+          }
+        }
+      }
     }
   }
   __syncthreads();
@@ -279,15 +347,28 @@ __global__ __launch_bounds__(256) void pack_frag_kernel(const T* __restrict__ B,
 }
 
 
+template <typename T, int NTI, int MS, bool RING>
+hipError_t launch_frag_t(const SmallPlan& p, const Args& a, const void* frag) {
+  const hipError_t attr = allow_lds<&small_frag_mfma_kernel<T, NTI, MS, RING>>();
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((small_frag_mfma_kernel<T, NTI, MS, RING>), dim3(p.grid),
+                     dim3(kFragThreads), p.lds, a.stream, (const T*)a.X, (const float4*)frag,
+                     (const T*)a.C, a.labels, a.scores, a.N, a.F, a.D, a.K, a.act, p.nblocks,
+                     p.cslots, (int)(p.lds / sizeof(float)), a.ws);
+  return hipGetLastError();
+}
+
+// The ring (reloads inside a loop) only where some workgroup walks more than
+// three blocks; the first workgroup of each XCD walks the most.
 template <typename T, int NTI, int MS>
 hipError_t launch_frag(const SmallPlan& p, const Args& a, const void* frag) {
-  const hipError_t attr = allow_lds<&small_frag_mfma_kernel<T, NTI, MS>>();
-  if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((small_frag_mfma_kernel<T, NTI, MS>), dim3(p.grid), dim3(kFragThreads), p.lds,
-                     a.stream, (const T*)a.X, (const float4*)frag, (const T*)a.C,
-                     a.labels, a.scores, a.N, a.F, a.D, a.K, a.act, p.nblocks, p.cslots,
-                     (int)(p.lds / sizeof(float)), a.ws);
-  return hipGetLastError();
+  int most = 0;
+  for (int x = 0; x < 8; ++x) {
+    const int c = block_walk(x, p.grid, p.nblocks).count();
+    most = c > most ? c : most;
+  }
+  return most > 3 ? launch_frag_t<T, NTI, MS, true>(p, a, frag)
+                  : launch_frag_t<T, NTI, MS, false>(p, a, frag);
 }
 
 template <typename T, int NTI>

@@ -212,6 +212,9 @@ INTEGER = [
     (32, 33, 1000, 5, "f32", False, "small_block_mfma_kernel"),
     (16, 561, 10240, 6, "f32", True, "small_frag_mfma_kernel"),
     (32, 561, 10240, 6, "f32", True, "small_frag_mfma_kernel"),
+    # more than three column blocks per workgroup: the fragment kernel's B ring
+    (32, 561, 20480, 6, "f32", True, "small_frag_mfma_kernel"),
+    (24, 1000, 13000, 5, "f32", True, "small_frag_mfma_kernel"),
     (48, 300, 2048, 16, "f32", True, "small_frag_mfma_kernel"),
     (64, 200, 1000, 12, "f32", True, "small_frag_mfma_kernel"),
     (64, 561, 4096, 6, "f32", True, "small_mfma_kernel"),
@@ -408,7 +411,10 @@ PACKED_SMALL = [(1, 561, 10240, 6, "f32"), (3, 20, 1000, 4, "f32"), (8, 1100, 77
                 (64, 1500, 513, 3, "bf16"), (17, 900, 333, 2, "f32"), (64, 200, 1000, 3, "f32"),
                 (12, 5, 64, 3, "f32"), (16, 4, 100, 2, "f32"), (48, 700, 2000, 26, "f32"),
                 (24, 300, 1000, 16, "f32"), (10, 100, 500, 13, "f32"),
-                (32, 561, 10240, 6, "bf16"), (16, 1023, 999, 16, "bf16"), (9, 5, 64, 2, "bf16")]
+                (32, 561, 10240, 6, "bf16"), (16, 1023, 999, 16, "bf16"), (9, 5, 64, 2, "bf16"),
+                # more than three column blocks per workgroup (the B ring)
+                (32, 561, 20480, 6, "f32"), (20, 1000, 16000, 3, "f32"),
+                (16, 300, 16384, 10, "bf16")]
 
 
 @pytest.mark.parametrize("N,F,D,K,dtype", PACKED_SMALL)
