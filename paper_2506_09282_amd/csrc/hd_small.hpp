@@ -37,11 +37,11 @@ __host__ __device__ inline SmallWs small_ws(void* ws) {
 }
 
 // Score replicas: enough that few workgroups add into each address (atomics
-// on one address are serialised), few enough that the finishing workgroup
-// reads all of them in one batch (R*N*K <= 16 per thread).
+// on one address are serialised), few enough that the finishing workgroup's
+// exchanges stay cheap: about 1024 replica values in all, at least 8 replicas.
 __host__ __device__ inline int replicas(int G, int NK) {
-  int r = (16 * 256) / (NK > 0 ? NK : 1);
-  r = r < 4 ? 4 : r > kSmallReplicas ? kSmallReplicas : r;
+  int r = 1024 / (NK > 0 ? NK : 1);
+  r = r < 8 ? 8 : r > kSmallReplicas ? kSmallReplicas : r;
   return G < r ? G : r;
 }
 

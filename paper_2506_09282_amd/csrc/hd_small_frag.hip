@@ -94,9 +94,9 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
 #pragma unroll
       for (int g = 0; g < G4; ++g) x.a[g] = p[g * stride];
     };
-    load_b(b0, 0);
-    load_b(b1, 1);  // the third block goes out after the barrier
-    __syncthreads();  // X and the blocks' C values are in LDS
+    load_b(b0, 0);  // blocks 1 and 2 go out after the barrier, so that X
+    __syncthreads();  // competes with one block of B only; X and C are in LDS
+    load_b(b1, 1);
 
     // X operands: they do not depend on the block, so when the registers
     // allow they are read from LDS once into registers (no LDS latency
