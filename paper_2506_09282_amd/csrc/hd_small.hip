@@ -94,19 +94,33 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay
   SmallPlan p{};
   p.nblocks = v.nblocks;
   if (lay == kTiled && dt <= 1 && x_aligned && N > 8 && frag_ms(F) > 0) {
-    const int nti = (int)cdiv(N, 16), ms = frag_ms(F);
-    const int64_t nbk = 16 * nti;
+    const int ms = frag_ms(F);
     int64_t cslots = 1;  // the most blocks any workgroup walks
     for (int b = 0; b < v.grid; ++b) {
       const int c = block_walk(b, v.grid, v.nblocks).count();
       cslots = c > cslots ? c : cslots;
     }
-    const int64_t floats = (nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 + cslots * K * kW +
-                           (nbk * F + 16 * ms + 3) / 4 * 4 + 4;
+    // LDS: scores of every sample, the partials, the blocks' C, one pass's X
+    auto frag_floats = [&](int64_t nti, int64_t npass) {
+      const int64_t nbk = 16 * nti;
+      return (npass * nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 + cslots * K * kW +
+             (nbk * F + 16 * ms + 3) / 4 * 4 + 4;
+    };
+    // all samples in one pass; else, when X of all of them does not fit and
+    // no workgroup walks more than three blocks (B stays in registers), two
+    // passes of 32
+    int64_t nti = cdiv(N, 16), npass = 1;
+    int64_t floats = frag_floats(nti, 1);
+    if ((int64_t)sizeof(float) * floats > kLdsBudget && N > 32 && cslots <= 3) {
+      nti = 2;
+      npass = 2;
+      floats = frag_floats(2, 2);
+    }
     if (K <= kFragMaxK && (int64_t)sizeof(float) * floats <= kLdsBudget) {
       p.frag = true;
+      p.npass = (int)npass;
       p.cslots = (int)cslots;
-      p.nb = nti;
+      p.nb = (int)nti;
       p.ms = ms;
       p.lds = sizeof(float) * (size_t)floats;
       p.grid = v.grid;
@@ -232,6 +246,7 @@ static SmallPlan plan_stream(int64_t N, int64_t F, int64_t D, int64_t K, int dt)
   // the reducer workgroup's eight per-wave sums use the same allocation
   if (floats < 8 * nbk * K || (int64_t)sizeof(float) * floats > kLdsBudget) return p;
   p.frag = true;
+  p.npass = 1;
   p.cslots = (int)cslots;
   p.nb = nti;
   p.ms = ms;

@@ -452,6 +452,7 @@ struct SmallPlan {
   bool bmfma;  // block matrix-core kernel (one block per workgroup, N <= 32)
   bool frag;   // fragment matrix-core kernel (packed model)
   int cslots;  // fragment kernel: C slots (blocks per workgroup)
+  int npass;   // fragment kernel: sample passes (2: two passes of 32, B kept in registers)
   bool mfma;
   int nb;    // VALU samples per pass, or MFMA sample tiles
   int ms;    // MFMA steps per wave

@@ -52,16 +52,21 @@ __device__ __forceinline__ float4 load4w(const bf16raw* p, int64_t i) {
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
 }
 
-template <typename T, int NTI, int MS, bool RING>
+template <typename T, int NTI, int MS, bool RING, int NPASS>
 __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     const T* __restrict__ X, const float4* __restrict__ Bf, const T* __restrict__ C,
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
     int nblocks, int cslots, int lds_floats, void* __restrict__ workspace) {
-  constexpr int NB = 16 * NTI;
+  static_assert(NPASS == 1 || !RING, "two sample passes keep every block of B in registers");
+  constexpr int NB = 16 * NTI;  // samples per pass
   constexpr int G4 = MS / 4;
+  // X operands: they do not depend on the block, so when the registers allow
+  // they are read from LDS once per pass into registers (no LDS latency
+  // between matrix instructions)
+  constexpr bool kXReg = 3 * MS + NTI * MS <= 180;
   extern __shared__ __attribute__((aligned(16))) float smem[];
-  float* sl = smem;                          // [NB*K]
-  float* red = sl + (NB * K + 3) / 4 * 4;    // [2][4][NTI][16][16]
+  float* sl = smem;                                  // [NPASS*NB*K]
+  float* red = sl + (NPASS * NB * K + 3) / 4 * 4;    // [2][4][NTI][16][16]
   float* cs = red + 2 * kWaves * NTI * 256;  // [cslots][K*16]: C of block i at slot i
   float* xs = cs + cslots * K * kW;          // [NB*F + 16*MS] + 4 spare
   const SmallWs ws = small_ws(workspace);
@@ -73,8 +78,6 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
   const bool det = (act & kActDet) != 0;
   act &= 1;
   const int R = det ? G : replicas(G, N * K);
-  const int nb = min(NB, N);
-  const int npairs = nb * K;
   const int nmine = walk.count();
 
   // The two roles run separate code paths from the first instruction, with
@@ -98,21 +101,20 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     __syncthreads();  // competes with one block of B only; X and C are in LDS
     load_b(b1, 1);
 
-    // X operands: they do not depend on the block, so when the registers
-    // allow they are read from LDS once into registers (no LDS latency
-    // between matrix instructions)
-    constexpr bool kXReg = 3 * MS + NTI * MS <= 180;
     const int xoff = (lane & 15) * F + 4 * MS * cw + MS * (lane >> 4);
     float4 xr[kXReg ? G4 : 1][kXReg ? NTI : 1];
-    if (kXReg) {
+    auto read_x = [&] {
+      if constexpr (kXReg) {
 #pragma unroll
-      for (int g = 0; g < (kXReg ? G4 : 1); ++g)
+        for (int g = 0; g < G4; ++g)
 #pragma unroll
-        for (int t = 0; t < (kXReg ? NTI : 1); ++t) {
-          const float* q = xs + xoff + 16 * t * F + 4 * g;
-          xr[g][t] = make_float4(q[0], q[1], q[2], q[3]);
-        }
-    }
+          for (int t = 0; t < NTI; ++t) {
+            const float* q = xs + xoff + 16 * t * F + 4 * g;
+            xr[g][t] = make_float4(q[0], q[1], q[2], q[3]);
+          }
+      }
+    };
+    read_x();
     load_b(b2, 2);
     auto multiply = [&](const FragBuf<MS>& x, int i) {
       // two independent accumulator chains per sample tile (steps 4g, 4g+2
@@ -161,16 +163,29 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
       // At most three blocks per workgroup: straight-line steps, no reloads.
       // Without a loop the compiler counts the outstanding loads exactly, so
       // step i waits only for block i (the ring's loop makes it wait for
-      // loads issued after block i as well).
-      multiply(b0, 0);
-      __syncthreads();
-      if (nmine > 1) {
-        multiply(b1, 1);
+      // loads issued after block i as well). A second pass of samples reuses
+      // the three blocks held in registers.
+#pragma unroll
+      for (int pass = 0; pass < NPASS; ++pass) {
+        if (pass > 0) {
+          __syncthreads();  // the finish waves' last step of the previous pass
+          __syncthreads();  // this pass's X is in LDS
+          read_x();
+        }
+        // Barriers: the finish waves take one for the first X, nmine + 1 per
+        // pass (their step loop) and one for each further pass's X; these
+        // waves take the first X's, nmine per pass, two between passes (the
+        // finish waves' last step, the next X) and one at the end.
+        multiply(b0, 0);
         __syncthreads();
-      }
-      if (nmine > 2) {
-        multiply(b2, 2);
-        __syncthreads();
+        if (nmine > 1) {
+          multiply(b1, 1);
+          __syncthreads();
+        }
+        if (nmine > 2) {
+          multiply(b2, 2);
+          __syncthreads();
+        }
       }
     } else {
       auto stepc = [&](FragBuf<MS>& b, int i) {
@@ -188,32 +203,57 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     }
     __syncthreads();  // the finish waves' last step
   } else {
-    // X copied verbatim into LDS (xs[n*F + f]). Each workgroup starts at a
-    // different offset so that they do not all read the same L2 lines at
-    // once; stores are unconditional (past the end they go to the spare
-    // slot) so that no load is sunk to its store. Steps past F read the next
-    // row (finite values times zero B) or, after the last row, the zeroed
-    // run of 16*MS floats.
-    const int n4 = nb * F / 4;
-    const int rot = (int)(((int64_t)blockIdx.x * 37 * 64) % n4);
+    // X copied verbatim into LDS (xs[n*F + f], the pass's rows). Each
+    // workgroup starts at a different offset so that they do not all read the
+    // same L2 lines at once; stores are unconditional (past the end they go
+    // to the spare slot) so that no load is sunk to its store. Steps past F
+    // read the next row (finite values times zero B) or, after the last row,
+    // the zeroed run of 16*MS floats. Rows of a pass start 16-byte aligned
+    // (NB*F floats per pass, NB a multiple of 16).
+    constexpr int kXB = NTI * MS / 4 < 40 ? NTI * MS / 4 : 40;
     float4* xs4 = reinterpret_cast<float4*>(xs);
     const int spare4 = (NB * F + 16 * MS + 3) / 4;
-    constexpr int kXB = NTI * MS / 4 < 40 ? NTI * MS / 4 : 40;
-    for (int base = 0; base < n4; base += kThreads * kXB) {
+    struct XBatch {
       float4 v[kXB];
       int at[kXB];
+    };
+    auto x_rows = [&](int pass) { return min(NB, N - NB * pass); };
+    // loads of one batch of the pass's float4s (base: first float4 index)
+    auto x_load = [&](XBatch& xb, int pass, int base) {
+      const T* Xp = X + (int64_t)NB * pass * F;
+      const int n4 = x_rows(pass) * F / 4;
+      const int rot = (int)(((int64_t)blockIdx.x * 37 * 64) % n4);
 #pragma unroll
       for (int j = 0; j < kXB; ++j) {
         const int i = base + j * kThreads + tid;
         const int r = i + rot >= n4 ? i + rot - n4 : i + rot;
-        at[j] = i < n4 ? r : spare4;
-        v[j] = load4w(X, i < n4 ? r : rot);
+        xb.at[j] = i < n4 ? r : spare4;
+        xb.v[j] = load4w(Xp, i < n4 ? r : rot);
       }
+    };
+    auto x_store = [&](const XBatch& xb) {
 #pragma unroll
-      for (int j = 0; j < kXB; ++j) xs4[at[j]] = v[j];
+      for (int j = 0; j < kXB; ++j) xs4[xb.at[j]] = xb.v[j];
+    };
+    // the rest of the pass after its first batch: further batches, the
+    // floats past the last whole float4, and the zeroed run
+    auto x_finish = [&](int pass) {
+      const T* Xp = X + (int64_t)NB * pass * F;
+      const int rows = x_rows(pass), n4 = rows * F / 4;
+      for (int base = kThreads * kXB; base < n4; base += kThreads * kXB) {
+        XBatch xb;
+        x_load(xb, pass, base);
+        x_store(xb);
+      }
+      for (int e = 4 * n4 + tid; e < rows * F; e += kThreads) xs[e] = load_elem(Xp, e);
+      for (int e = tid; e < 16 * MS; e += kThreads) xs[rows * F + e] = 0.0f;
+    };
+    {
+      XBatch xb;
+      x_load(xb, 0, 0);
+      x_store(xb);
     }
-    for (int e = 4 * n4 + tid; e < nb * F; e += kThreads) xs[e] = load_elem(X, e);
-    for (int e = tid; e < 16 * MS; e += kThreads) xs[nb * F + e] = 0.0f;
+    x_finish(0);
     // block i's K*16 C values are one contiguous run of the column tiles
     const int kc4 = K * kW / 4;
     for (int e = tid; e < nmine * kc4; e += kThreads) {
@@ -254,7 +294,7 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
         v[0] = *p;
       }
     };
-    auto finish = [&](int i) {
+    auto finish = [&](int i, int nb) {
       if (fn >= nb) return;  // a sample's lanes drop out together
       // red[i % 2][w][t][n16][16 d]: sample fn = 16 t + n16 is row fn of wave w's part
       const float* r = red + (i & 1) * kWaves * NTI * 256 + fn * 16 + fc;
@@ -286,17 +326,11 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
         }
       }
     };
-    // Step i (one barrier each, nmine + 1 steps): finish block i-1 while the
-    // compute waves multiply block i.
-    for (int i = 0; i <= nmine; ++i) {
-      if (i > 0) finish(i - 1);
-      __syncthreads();
-    }
-    // The sample's LPS lanes are consecutive, aligned and drop out together.
-    // DPP sums them without LDS traffic: the two quad swaps leave each quad's
-    // total in its lanes, the half-row mirror (lane l of 8 reads lane 7-l)
-    // adds the other quad of 8, the row mirror (l of 16 reads 15-l) the other
-    // half-row; every lane then holds its sample's total.
+    // Step i (one barrier each, nmine + 1 steps per pass): finish block i-1
+    // while the compute waves multiply block i. With a second pass, its X is
+    // requested at the start of the first pass and stored once the compute
+    // waves no longer read the first pass's X: after step 0 when they hold X
+    // in registers, else after the pass.
     auto dpp_add = [](float d, auto ctrl) {
       return d + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
                                                0, __builtin_bit_cast(int, d), decltype(ctrl)::value,
@@ -306,24 +340,51 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     using QuadSwap2 = std::integral_constant<int, 0x4E>;  // quad_perm [2,3,0,1]
     using HalfMirror = std::integral_constant<int, 0x141>;  // row_half_mirror
     using RowMirror = std::integral_constant<int, 0x140>;   // row_mirror
-    if (fn < nb) {
 #pragma unroll
-      for (int kg = 0; kg < kFragMaxK / 4; ++kg) {
-        if (4 * kg < K) {
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int nb = x_rows(pass);
+      XBatch next;
+      const bool more = pass + 1 < NPASS;
+      if (more) x_load(next, pass + 1, 0);
+      const bool early = more && kXReg && nmine >= 1;
+      for (int i = 0; i <= nmine; ++i) {
+        if (i > 0) finish(i - 1, nb);
+        if (early && i == 1) x_store(next);
+        __syncthreads();
+      }
+      // The sample's LPS lanes are consecutive, aligned and drop out
+      // together. DPP sums them without LDS traffic: the two quad swaps leave
+      // each quad's total in its lanes, the half-row mirror (lane l of 8
+      // reads lane 7-l) adds the other quad of 8, the row mirror (l of 16
+      // reads 15-l) the other half-row; every lane then holds its sample's
+      // total.
+      if (fn < nb) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int k = 4 * kg + j;
-            float d = dpp_add(dpp_add(psum[k], QuadSwap1{}), QuadSwap2{});
-            if constexpr (LPS >= 8) d = dpp_add(d, HalfMirror{});
-            if constexpr (LPS >= 16) d = dpp_add(d, RowMirror{});
-            if (k < K && tid % LPS == k % LPS) sl[fn * K + k] = d;
+        for (int kg = 0; kg < kFragMaxK / 4; ++kg) {
+          if (4 * kg < K) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int k = 4 * kg + j;
+              float d = dpp_add(dpp_add(psum[k], QuadSwap1{}), QuadSwap2{});
+              if constexpr (LPS >= 8) d = dpp_add(d, HalfMirror{});
+              if constexpr (LPS >= 16) d = dpp_add(d, RowMirror{});
+              if (k < K && tid % LPS == k % LPS) sl[(NB * pass + fn) * K + k] = d;
+            }
           }
         }
+      }
+      if (more) {
+#pragma unroll
+        for (int k = 0; k < kFragMaxK; ++k) psum[k] = 0.0f;
+        if (!early) x_store(next);
+        x_finish(pass + 1);
+        __syncthreads();  // the next pass's X is in LDS
       }
     }
   }
   __syncthreads();
-  publish_and_finish<kFragThreads>(sl, 0, nb, N, K, R, ws, labels, scores, smem, lds_floats,
+  publish_and_finish<kFragThreads>(sl, 0, min(NPASS * NB, N), N, K, R, ws, labels, scores, smem,
+                                   lds_floats,
                                    true, det);
 }
 
@@ -347,11 +408,11 @@ __global__ __launch_bounds__(256) void pack_frag_kernel(const T* __restrict__ B,
 }
 
 
-template <typename T, int NTI, int MS, bool RING>
+template <typename T, int NTI, int MS, bool RING, int NPASS>
 hipError_t launch_frag_t(const SmallPlan& p, const Args& a, const void* frag) {
-  const hipError_t attr = allow_lds<&small_frag_mfma_kernel<T, NTI, MS, RING>>();
+  const hipError_t attr = allow_lds<&small_frag_mfma_kernel<T, NTI, MS, RING, NPASS>>();
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((small_frag_mfma_kernel<T, NTI, MS, RING>), dim3(p.grid),
+  hipLaunchKernelGGL((small_frag_mfma_kernel<T, NTI, MS, RING, NPASS>), dim3(p.grid),
                      dim3(kFragThreads), p.lds, a.stream, (const T*)a.X, (const float4*)frag,
                      (const T*)a.C, a.labels, a.scores, a.N, a.F, a.D, a.K, a.act, p.nblocks,
                      p.cslots, (int)(p.lds / sizeof(float)), a.ws);
@@ -359,16 +420,22 @@ hipError_t launch_frag_t(const SmallPlan& p, const Args& a, const void* frag) {
 }
 
 // The ring (reloads inside a loop) only where some workgroup walks more than
-// three blocks; the first workgroup of each XCD walks the most.
+// three blocks; the first workgroup of each XCD walks the most. Two sample
+// passes (planned only without the ring) for 32 < N <= 64 when X of all the
+// samples does not fit LDS.
 template <typename T, int NTI, int MS>
 hipError_t launch_frag(const SmallPlan& p, const Args& a, const void* frag) {
+  if constexpr (NTI == 2) {
+    if (p.npass == 2) return launch_frag_t<T, 2, MS, false, 2>(p, a, frag);
+  }
+  if (p.npass != 1) return hipErrorInvalidValue;
   int most = 0;
   for (int x = 0; x < 8; ++x) {
     const int c = block_walk(x, p.grid, p.nblocks).count();
     most = c > most ? c : most;
   }
-  return most > 3 ? launch_frag_t<T, NTI, MS, true>(p, a, frag)
-                  : launch_frag_t<T, NTI, MS, false>(p, a, frag);
+  return most > 3 ? launch_frag_t<T, NTI, MS, true, 1>(p, a, frag)
+                  : launch_frag_t<T, NTI, MS, false, 1>(p, a, frag);
 }
 
 template <typename T, int NTI>

@@ -33,7 +33,7 @@ CASES = [
     (64, 33, 1000, 5, "f32", False, "small_mfma_kernel"),
     (32, 561, 10240, 6, "f32", True, "small_frag_mfma_kernel"),
     (64, 617, 10240, 26, "f32", True, "small_valu_kernel"),
-    (200, 561, 10240, 6, "f32", True, "small_mfma_kernel"),
+    (200, 561, 10240, 6, "f32", True, "small_frag_mfma_kernel"),  # 64-sample calls, two passes
     (32, 561, 10240, 6, "bf16", True, "small_frag_mfma_kernel"),
     (16, 617, 4096, 26, "bf16", True, "large_fused_kernel"),
     (16, 3072, 1000, 5, "bf16", False, "large_chunked_dma_kernel"),

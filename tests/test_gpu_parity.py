@@ -217,7 +217,9 @@ INTEGER = [
     (24, 1000, 13000, 5, "f32", True, "small_frag_mfma_kernel"),
     (48, 300, 2048, 16, "f32", True, "small_frag_mfma_kernel"),
     (64, 200, 1000, 12, "f32", True, "small_frag_mfma_kernel"),
-    (64, 561, 4096, 6, "f32", True, "small_mfma_kernel"),
+    (64, 561, 4096, 6, "f32", True, "small_frag_mfma_kernel"),  # two passes of 32 samples
+    (50, 1000, 10240, 6, "f32", True, "small_frag_mfma_kernel"),  # two passes, ragged second
+    (64, 561, 20480, 6, "f32", True, "small_mfma_kernel"),
     (64, 100, 2048, 17, "f32", False, "small_mfma_kernel"),
     (65, 100, 2048, 17, "f32", False, None),
     (300, 617, 4096, 26, "f32", False, "large_fused_kernel"),
@@ -258,6 +260,7 @@ TIES = [
     (5, 40, 512, "bf16", False, "small_flat_kernel"),
     (200, 40, 512, "bf16", False, "large_fused_kernel"),
     (32, 40, 512, "f32", True, "small_frag_mfma_kernel"),
+    (64, 700, 4096, "f32", True, "small_frag_mfma_kernel"),  # two sample passes
     (64, 200, 1024, "f32", True, "small_frag_mfma_kernel"),
     (100, 2560, 512, "bf16", True, "large_chunked_dma_kernel"),
     (32, 40, 512, "bf16", True, "small_frag_mfma_kernel"),
@@ -414,7 +417,10 @@ PACKED_SMALL = [(1, 561, 10240, 6, "f32"), (3, 20, 1000, 4, "f32"), (8, 1100, 77
                 (32, 561, 10240, 6, "bf16"), (16, 1023, 999, 16, "bf16"), (9, 5, 64, 2, "bf16"),
                 # more than three column blocks per workgroup (the B ring)
                 (32, 561, 20480, 6, "f32"), (20, 1000, 16000, 3, "f32"),
-                (16, 300, 16384, 10, "bf16")]
+                (16, 300, 16384, 10, "bf16"),
+                # two passes of 32 samples (X of all samples exceeds LDS)
+                (64, 561, 10240, 6, "f32"), (37, 900, 8000, 11, "f32"),
+                (64, 561, 10240, 6, "bf16"), (45, 700, 3000, 16, "bf16")]
 
 
 @pytest.mark.parametrize("N,F,D,K,dtype", PACKED_SMALL)
