@@ -40,6 +40,15 @@ constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 // f-steps of B fragments in flight per wave: deeper while registers allow
 constexpr int prefetch_of(int ntiles, int kb) { return ntiles * kb <= 4 ? 8 : 4; }
+// Ring depth of the int8 resident-X kernel where 8 would be used: a unit's
+// f-steps run in groups of the depth, the last group padded with zero X, and
+// int8's 32-row f-steps leave few steps per unit, so take 10 when it pads
+// fewer steps. The depth must be even: the X fragments are double-buffered by
+// the step's index within its group.
+constexpr int fused_prefetch(int nfs) {
+  const int pad8 = (nfs + 7) / 8 * 8 - nfs, pad10 = (nfs + 9) / 10 * 10 - nfs;
+  return pad10 < pad8 ? 10 : 8;
+}
 constexpr int kMaxSlices = 64;  // D slices per sample tile (split-D)
 constexpr int kLdsBytes = 160 * 1024 - 256;  // leave room for static LDS
 
@@ -561,14 +570,15 @@ __device__ void finish_tile(f32x16 (&sacc)[NTILES][KB], unsigned char* lds, int*
 // ---------------------------------------------------------------------------
 // The fused kernel.
 // ---------------------------------------------------------------------------
-template <class Tr, int NTILES, int KB, int ACT>
+template <class Tr, int NTILES, int KB, int ACT, int PF>
 __global__ __launch_bounds__(kThreads, 1) void large_fused_kernel(
     const typename Tr::elem* __restrict__ X, const uint4* __restrict__ Bp,
     const uint4* __restrict__ Cp, int32_t* __restrict__ labels, float* __restrict__ scores,
     int N, int F, int K, int ndb, int DS, void* __restrict__ workspace) {
   typedef typename Tr::elem T;
   constexpr int NT = 32 * NTILES;
-  constexpr int kPrefetch = prefetch_of(NTILES, KB);
+  static_assert(PF % 2 == 0, "X fragments are double-buffered by step parity");
+  constexpr int kPrefetch = PF;  // B ring depth in f-steps
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   __shared__ int s_last;
 
@@ -1737,6 +1747,19 @@ hipError_t allow_large_lds() {
   });
 }
 
+template <class Tr, int NTILES, int KB, int ACT, int PF>
+hipError_t launch_fused(const LargeCfg& c, const void* X, const uint4* Bp, const uint4* Cp,
+                        int32_t* labels, float* scores, int64_t N, int64_t F, int64_t K, int ndb,
+                        void* ws, hipStream_t stream) {
+  const dim3 grid((unsigned)(c.ntiles * c.ds)), block(kThreads);
+  const hipError_t attr = allow_large_lds<&large_fused_kernel<Tr, NTILES, KB, ACT, PF>>();
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((large_fused_kernel<Tr, NTILES, KB, ACT, PF>), grid, block, c.lds, stream,
+                     (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F, (int)K,
+                     ndb, c.ds, ws);
+  return hipGetLastError();
+}
+
 template <class Tr, int NTILES, int KB, int ACT>
 hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const uint4* Cp,
                       int32_t* labels, float* scores, int64_t N, int64_t F, int64_t K, int ndb,
@@ -1765,12 +1788,14 @@ hipError_t launch_act(const LargeCfg& c, const void* X, const uint4* Bp, const u
     }
     return hipErrorInvalidValue;
   }
-  const hipError_t attr = allow_large_lds<&large_fused_kernel<Tr, NTILES, KB, ACT>>();
-  if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((large_fused_kernel<Tr, NTILES, KB, ACT>), grid, block, c.lds, stream,
-                     (const typename Tr::elem*)X, Bp, Cp, labels, scores, (int)N, (int)F, (int)K,
-                     ndb, c.ds, ws);
-  return hipGetLastError();
+  constexpr int kPF = prefetch_of(NTILES, KB);
+  if constexpr (kPF == 8 && ACT == 0 && Tr::kEsz == 1) {
+    if (fused_prefetch(nfs_of<Tr>((int)F)) == 10)
+      return launch_fused<Tr, NTILES, KB, ACT, 10>(c, X, Bp, Cp, labels, scores, N, F, K, ndb,
+                                                   ws, stream);
+  }
+  return launch_fused<Tr, NTILES, KB, ACT, kPF>(c, X, Bp, Cp, labels, scores, N, F, K, ndb, ws,
+                                                stream);
 }
 
 template <class Tr, int NTILES, int KB>
