@@ -35,13 +35,16 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 //   several passes over B (40 us at N = 16, 72 us at N = 32), the matrix-core
 //   path takes 34 us at N = 16..32; a packed bf16 model instead carries fp32
 //   fragments (bf16 widened exactly) and takes the fragment kernel;
-// * fp32 with 64 < N <= 256: the matrix-core path has only a few sample tiles
-//   (138 us for N = 65..256), while the small path takes about 32 us per 64
-//   samples, so it runs in 64-sample chunks, one after another on the stream,
-//   when its 64-sample plan runs on the matrix cores (not the VALU fallback).
+// * 64 < N <= 256 in fp32, 64 < N <= 128 on a packed bf16 model: the
+//   matrix-core path has only a few sample tiles (fp32: 138 us for
+//   N = 65..256; bf16: 39 us at N = 65, 46 us at N = 128), while the small path
+//   takes about 20 us per 64 samples, so it runs in 64-sample chunks, one
+//   after another on the stream, when its 64-sample plan runs on the matrix
+//   cores (not the VALU fallback).
 enum class Route { kSmall, kSmallChunked, kLarge, kNone };
 constexpr int64_t kSmallMaxNBf16 = 8;
 constexpr int64_t kChunkedMaxN = 256;
+constexpr int64_t kChunkedMaxNBf16 = 128;  // a packed bf16 model's fragment kernel
 
 Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   if (dt == HD_I8) return hd::large_supported(N, F, D, K, dt) ? Route::kLarge : Route::kNone;
@@ -51,6 +54,9 @@ Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   if (small_ok && dt == HD_BF16 && tiled && hd::small_matrix_core(N, F, D, K, dt, tiled))
     return Route::kSmall;
   if (dt == HD_F32 && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
+      hd::small_matrix_core(hd::kSmallMaxN, F, D, K, dt, tiled))
+    return Route::kSmallChunked;
+  if (dt == HD_BF16 && tiled && N > hd::kSmallMaxN && N <= kChunkedMaxNBf16 &&
       hd::small_matrix_core(hd::kSmallMaxN, F, D, K, dt, tiled))
     return Route::kSmallChunked;
   if (hd::large_supported(N, F, D, K, dt)) return Route::kLarge;

@@ -229,6 +229,10 @@ def test_routes_of_new_paths(L):
     assert k(32, 561, 10240, 6, hd.HD_BF16, 1) == b"small_frag_mfma_kernel"
     assert k(32, 561, 10240, 6, hd.HD_BF16, 0) == b"large_fused_kernel"
     assert k(32, 561, 10240, 17, hd.HD_BF16, 1) == b"large_fused_kernel"  # K > 16
+    # 64-sample calls of the fragment kernel up to 128 samples of a packed bf16 model
+    assert k(128, 561, 10240, 6, hd.HD_BF16, 1) == b"small_frag_mfma_kernel"
+    assert k(129, 561, 10240, 6, hd.HD_BF16, 1) == b"large_fused_kernel"
+    assert k(100, 561, 10240, 6, hd.HD_BF16, 0) == b"large_fused_kernel"
     b = L.hd_bundle_kernel
     assert b(16384, 3072, 10240, 10, hd.HD_BF16, 1) == b"bundle_dma_kernel"
     assert b(16384, 3072, 10240, 10, hd.HD_I8, 1) == b"bundle_dma_kernel"
