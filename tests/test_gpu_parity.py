@@ -225,6 +225,7 @@ INTEGER = [
     (300, 617, 4096, 26, "f32", False, "large_fused_kernel"),
     (300, 617, 4096, 26, "bf16", True, "large_fused_kernel"),
     (257, 31, 700, 3, "bf16", False, "large_fused_kernel"),
+    (300, 784, 2048, 10, "bf16", True, "large_fused_kernel"),
     (32, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),
     (16, 561, 10240, 6, "bf16", True, "small_frag_mfma_kernel"),
     (40, 301, 1000, 16, "bf16", True, "small_frag_mfma_kernel"),
@@ -258,6 +259,7 @@ TIES = [
     (5, 40, 512, "f32", False, "small_flat_kernel"),
     (200, 40, 512, "f32", False, "small_mfma_kernel"),
     (300, 40, 512, "f32", False, "large_fused_kernel"),
+    (250, 700, 512, "bf16", True, "large_fused_kernel"),
     (5, 40, 512, "bf16", False, "small_flat_kernel"),
     (200, 40, 512, "bf16", False, "large_fused_kernel"),
     (32, 40, 512, "f32", True, "small_frag_mfma_kernel"),
