@@ -77,8 +77,10 @@ int frag_ms(int64_t F) {
 }
 
 size_t frag_bytes(int64_t F, int64_t D, int dt) {
-  // fp32 fragments for fp32 and bf16 models (bf16 B widened exactly)
+  // fp32: MS/4 float4 per lane, wave and block; bf16: ceil(MS/8) words of
+  // eight bf16 (the bf16 matrix instruction's operands)
   const int ms = dt <= 1 ? frag_ms(F) : 0;
+  if (dt == 1) return (size_t)cdiv(D, kW) * 4 * ((ms + 7) / 8) * 64 * 16;
   return (size_t)cdiv(D, kW) * 256 * ms * sizeof(float);
 }
 
@@ -101,10 +103,13 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay
       cslots = c > cslots ? c : cslots;
     }
     // LDS: scores of every sample, the partials, the blocks' C, one pass's X
+    // (fp32: NB*F + 16*MS floats and a spare float4; bf16: NB*F + 32*MS
+    // bf16 and a spare word)
     auto frag_floats = [&](int64_t nti, int64_t npass) {
       const int64_t nbk = 16 * nti;
-      return (npass * nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 + cslots * K * kW +
-             (nbk * F + 16 * ms + 3) / 4 * 4 + 4;
+      const int64_t xf = dt == 1 ? ((nbk * F + 32 * ms + 7) / 8 + 1) * 4
+                                 : (nbk * F + 16 * ms + 3) / 4 * 4 + 4;
+      return (npass * nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 + cslots * K * kW + xf;
     };
     // all samples in one pass; else, when X of all of them does not fit and
     // no workgroup walks more than three blocks (B stays in registers), two

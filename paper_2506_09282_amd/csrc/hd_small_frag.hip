@@ -9,17 +9,24 @@ namespace sp {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Fragment matrix-core kernel (8 < N <= 64, packed model; fp32, or bf16
-// inputs widened exactly to fp32: a bf16 model's image carries this fp32
-// fragment section, and X and C are widened as they are staged). The packed
-// model holds, per 16-column block, the 16x16x4 A operands in the order the
-// waves consume them (see pack_frag_kernel): compute wave w's lane
-// l = (d, q), d = l % 16, q = l / 16, covers the MS consecutive rows
-// f = 4*MS*w + MS*q + 0..MS-1 of column 16 blk + d, four rows per float4, so
-// a block costs each lane MS/4 16-byte loads and each wave-wide load is one
-// contiguous 1 KiB run. Matrix step s of the wave multiplies row
-// 4*MS*w + MS*q + s (lane group q) with the same rows of X^T, read from a
-// verbatim copy of X in LDS.
+// Fragment matrix-core kernel (8 < N <= 64, packed model). Compute wave w
+// owns the 4*MS rows f = 4*MS*w .. 4*MS*w + 4*MS - 1 of F.
+//   fp32: the packed model holds, per 16-column block, the 16x16x4 A operands
+//     in the order the waves consume them (see pack_frag_kernel): lane
+//     l = (d, q), d = l % 16, q = l / 16, covers the MS consecutive rows
+//     f = 4*MS*w + MS*q + 0..MS-1 of column 16 blk + d, four rows per float4,
+//     so a block costs each lane MS/4 16-byte loads and each wave-wide load
+//     is one contiguous 1 KiB run. Matrix step s multiplies row
+//     4*MS*w + MS*q + s (lane group q) with the same rows of X^T, read from a
+//     verbatim copy of X in LDS.
+//   bf16: the A operands of v_mfma_f32_16x16x32_bf16 (see pack_frag16_kernel):
+//     step s of wave w, lane (d, q) holds the eight bf16 of rows
+//     f = 4*MS*w + 32*s + 8*q + 0..7 of column 16 blk + d (zero past the
+//     wave's rows or F), S16 = ceil(MS/8) steps, one 16-byte load each; X is
+//     staged in LDS as bf16 and each lane's eight X values are assembled
+//     from aligned dwords. The matrix instruction's k index is the same
+//     row of both operands, and its 16x16 result has the fp32 instruction's
+//     layout, so everything after the matrix steps is shared.
 //
 // Persistent, one 512-thread workgroup per CU walking its column blocks,
 // with the waves split by role so that memory, matrix and reduction work
@@ -33,13 +40,17 @@ namespace {
 //     i-1's partials into HardSign values and per-pair partial scores
 //     (Eq. 1, Eq. 8).
 // One barrier per block hands red from one role to the other.
-// LDS: sl[NB*K] | red[2][4 waves][NTI][16 n][16 d] | cs[cslots][K*16] |
-//      xs[NB*F + 16*MS] (+ 4 spare), cslots >= blocks per workgroup
+// LDS: sl[NPASS*NB*K] | red[2][4 waves][NTI][16 n][16 d] | cs[cslots][K*16] |
+//      xs: fp32 [NB*F + 16*MS] (+ 4 spare), bf16 [NB*F + 32*MS] (+ 8 spare);
+//      cslots >= blocks per workgroup
 // ---------------------------------------------------------------------------
 
-template <int MS>
+// One block's A operands per lane: MS/4 float4 (fp32) or ceil(MS/8) uint4
+// (eight bf16 each).
+template <int MS, bool N16>
 struct FragBuf {
-  float4 a[MS / 4];
+  using Word = std::conditional_t<N16, uint4, float4>;
+  Word a[N16 ? (MS + 7) / 8 : MS / 4];
 };
 
 // Four consecutive elements starting at element 4*i (16-byte or 8-byte aligned), as fp32.
@@ -58,17 +69,20 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
     int nblocks, int cslots, int lds_floats, void* __restrict__ workspace) {
   static_assert(NPASS == 1 || !RING, "two sample passes keep every block of B in registers");
+  constexpr bool N16 = std::is_same_v<T, bf16raw>;  // bf16 operands
   constexpr int NB = 16 * NTI;  // samples per pass
   constexpr int G4 = MS / 4;
+  constexpr int S16 = (MS + 7) / 8;
+  constexpr int NW = N16 ? S16 : G4;  // 16-byte A operand words per lane per block
   // X operands: they do not depend on the block, so when the registers allow
   // they are read from LDS once per pass into registers (no LDS latency
   // between matrix instructions)
-  constexpr bool kXReg = 3 * MS + NTI * MS <= 180;
+  constexpr bool kXReg = N16 ? 12 * S16 + 4 * S16 * NTI <= 180 : 3 * MS + NTI * MS <= 180;
   extern __shared__ __attribute__((aligned(16))) float smem[];
   float* sl = smem;                                  // [NPASS*NB*K]
   float* red = sl + (NPASS * NB * K + 3) / 4 * 4;    // [2][4][NTI][16][16]
   float* cs = red + 2 * kWaves * NTI * 256;  // [cslots][K*16]: C of block i at slot i
-  float* xs = cs + cslots * K * kW;          // [NB*F + 16*MS] + 4 spare
+  float* xs = cs + cslots * K * kW;          // X of one pass (fp32 or bf16)
   const SmallWs ws = small_ws(workspace);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool compute = wave >= kWaves;
@@ -89,63 +103,92 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     // B fragments of blocks 0, 1, 2. Blocks past the workgroup's last one
     // are "loaded" from a single broadcast address (one 16-byte request per
     // wave instruction), so the load count per step never depends on a branch.
-    FragBuf<MS> b0, b1, b2;
-    auto load_b = [&](FragBuf<MS>& x, int i) {
-      const float4* p = i < nmine
-          ? Bf + ((int64_t)walk.block_of(i) * kWaves + cw) * G4 * kWave + lane : Bf;
+    using Buf = FragBuf<MS, N16>;
+    using Word = typename Buf::Word;
+    const Word* Bw = reinterpret_cast<const Word*>(Bf);
+    Buf b0, b1, b2;
+    auto load_b = [&](Buf& x, int i) {
+      const Word* p = i < nmine
+          ? Bw + ((int64_t)walk.block_of(i) * kWaves + cw) * NW * kWave + lane : Bw;
       const int stride = i < nmine ? kWave : 0;
 #pragma unroll
-      for (int g = 0; g < G4; ++g) x.a[g] = p[g * stride];
+      for (int g = 0; g < NW; ++g) x.a[g] = p[g * stride];
     };
     load_b(b0, 0);  // blocks 1 and 2 go out after the barrier, so that X
     __syncthreads();  // competes with one block of B only; X and C are in LDS
     load_b(b1, 1);
 
-    const int xoff = (lane & 15) * F + 4 * MS * cw + MS * (lane >> 4);
-    float4 xr[kXReg ? G4 : 1][kXReg ? NTI : 1];
+    // fp32: this lane's X^T rows start at xoff; bf16: its eight X values of
+    // step s, tile t start at element xoff + 16*t*F + 32*s
+    const int xoff = N16 ? (lane & 15) * F + 4 * MS * cw + 8 * (lane >> 4)
+                         : (lane & 15) * F + 4 * MS * cw + MS * (lane >> 4);
+    // eight consecutive bf16 X values from element e: the five dwords that
+    // hold elements e - e % 2 .. e + 9, realigned by 0 or 2 bytes
+    auto x16 = [&](int e) {
+      const uint32_t* q = reinterpret_cast<const uint32_t*>(xs) + (e >> 1);
+      const uint32_t w0 = q[0], w1 = q[1], w2 = q[2], w3 = q[3], w4 = q[4];
+      const uint32_t sh = (uint32_t)(e & 1) * 2;
+      return make_uint4(__builtin_amdgcn_alignbyte(w1, w0, sh), __builtin_amdgcn_alignbyte(w2, w1, sh),
+                        __builtin_amdgcn_alignbyte(w3, w2, sh), __builtin_amdgcn_alignbyte(w4, w3, sh));
+    };
+    using XWord = std::conditional_t<N16, uint4, float4>;
+    XWord xr[kXReg ? NW : 1][kXReg ? NTI : 1];
+    auto x_word = [&](int g, int t) -> XWord {
+      if constexpr (N16) {
+        return x16(xoff + 16 * t * F + 32 * g);
+      } else {
+        const float* q = xs + xoff + 16 * t * F + 4 * g;
+        return make_float4(q[0], q[1], q[2], q[3]);
+      }
+    };
     auto read_x = [&] {
       if constexpr (kXReg) {
 #pragma unroll
-        for (int g = 0; g < G4; ++g)
+        for (int g = 0; g < NW; ++g)
 #pragma unroll
-          for (int t = 0; t < NTI; ++t) {
-            const float* q = xs + xoff + 16 * t * F + 4 * g;
-            xr[g][t] = make_float4(q[0], q[1], q[2], q[3]);
-          }
+          for (int t = 0; t < NTI; ++t) xr[g][t] = x_word(g, t);
       }
     };
     read_x();
     load_b(b2, 2);
-    auto multiply = [&](const FragBuf<MS>& x, int i) {
-      // two independent accumulator chains per sample tile (steps 4g, 4g+2
-      // and 4g+1, 4g+3), interleaved over the tiles
+    auto multiply = [&](const Buf& x, int i) {
+      // two independent accumulator chains per sample tile, interleaved over
+      // the tiles (fp32: steps 4g, 4g+2 and 4g+1, 4g+3; bf16: even and odd
+      // 32-row steps)
       f32x4 acc[NTI][2];
 #pragma unroll
       for (int t = 0; t < NTI; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int g = 0; g < G4; ++g) {
-        float4 xg[NTI];
+      for (int g = 0; g < NW; ++g) {
+        XWord xg[NTI];
 #pragma unroll
         for (int t = 0; t < NTI; ++t) {
           if constexpr (kXReg) {
             xg[t] = xr[g][t];
           } else {
-            const float* q = xs + xoff + 16 * t * F + 4 * g;
-            xg[t] = make_float4(q[0], q[1], q[2], q[3]);
+            xg[t] = x_word(g, t);
           }
         }
+        if constexpr (N16) {
 #pragma unroll
-        for (int t = 0; t < NTI; ++t)
-          acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].x, xg[t].x, acc[t][0], 0, 0, 0);
+          for (int t = 0; t < NTI; ++t)
+            acc[t][g & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, x.a[g]), __builtin_bit_cast(bf16x8, xg[t]),
+                acc[t][g & 1], 0, 0, 0);
+        } else {
 #pragma unroll
-        for (int t = 0; t < NTI; ++t)
-          acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].y, xg[t].y, acc[t][1], 0, 0, 0);
+          for (int t = 0; t < NTI; ++t)
+            acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].x, xg[t].x, acc[t][0], 0, 0, 0);
 #pragma unroll
-        for (int t = 0; t < NTI; ++t)
-          acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].z, xg[t].z, acc[t][0], 0, 0, 0);
+          for (int t = 0; t < NTI; ++t)
+            acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].y, xg[t].y, acc[t][1], 0, 0, 0);
 #pragma unroll
-        for (int t = 0; t < NTI; ++t)
-          acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].w, xg[t].w, acc[t][1], 0, 0, 0);
+          for (int t = 0; t < NTI; ++t)
+            acc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].z, xg[t].z, acc[t][0], 0, 0, 0);
+#pragma unroll
+          for (int t = 0; t < NTI; ++t)
+            acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].w, xg[t].w, acc[t][1], 0, 0, 0);
+        }
       }
       // lane l holds V^T[d = 4(l/16) + q][n = l%16], q = 0..3: one 16-byte
       // store into red[i % 2][cw][t][n][d]
@@ -188,7 +231,7 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
         }
       }
     } else {
-      auto stepc = [&](FragBuf<MS>& b, int i) {
+      auto stepc = [&](Buf& b, int i) {
         multiply(b, i);
         load_b(b, i + 3);
         __syncthreads();
@@ -210,43 +253,60 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     // read the next row (finite values times zero B) or, after the last row,
     // the zeroed run of 16*MS floats. Rows of a pass start 16-byte aligned
     // (NB*F floats per pass, NB a multiple of 16).
-    constexpr int kXB = NTI * MS / 4 < 40 ? NTI * MS / 4 : 40;
-    float4* xs4 = reinterpret_cast<float4*>(xs);
-    const int spare4 = (NB * F + 16 * MS + 3) / 4;
+    // X moves in 16-byte words: four fp32 or eight bf16 elements (bf16 X is
+    // staged as it is, fp32 the same)
+    using SWord = std::conditional_t<N16, uint4, float4>;
+    constexpr int EPW = N16 ? 8 : 4;    // elements per word
+    constexpr int ZRUN = N16 ? 32 * MS : 16 * MS;  // zeroed elements after the rows
+    // words per thread for NB rows of up to 16*MS elements: NB*16*MS / (EPW * 256)
+    constexpr int kXBw = (NTI * MS + EPW - 1) / EPW;
+    constexpr int kXB = kXBw < 40 ? kXBw : 40;
+    SWord* xsw = reinterpret_cast<SWord*>(xs);
+    const int spare = (NB * F + ZRUN + EPW - 1) / EPW;
     struct XBatch {
-      float4 v[kXB];
+      SWord v[kXB];
       int at[kXB];
     };
     auto x_rows = [&](int pass) { return min(NB, N - NB * pass); };
-    // loads of one batch of the pass's float4s (base: first float4 index)
+    // loads of one batch of the pass's words (base: first word index)
     auto x_load = [&](XBatch& xb, int pass, int base) {
       const T* Xp = X + (int64_t)NB * pass * F;
-      const int n4 = x_rows(pass) * F / 4;
-      const int rot = (int)(((int64_t)blockIdx.x * 37 * 64) % n4);
+      const int nw = x_rows(pass) * F / EPW;
+      const int rot = nw > 0 ? (int)(((int64_t)blockIdx.x * 37 * 64) % nw) : 0;
 #pragma unroll
       for (int j = 0; j < kXB; ++j) {
         const int i = base + j * kThreads + tid;
-        const int r = i + rot >= n4 ? i + rot - n4 : i + rot;
-        xb.at[j] = i < n4 ? r : spare4;
-        xb.v[j] = load4w(Xp, i < n4 ? r : rot);
+        const int r = i + rot >= nw ? i + rot - nw : i + rot;
+        xb.at[j] = i < nw ? r : spare;
+        if constexpr (N16)
+          xb.v[j] = reinterpret_cast<const uint4*>(Xp)[i < nw ? r : 0];
+        else
+          xb.v[j] = load4w(Xp, i < nw ? r : rot);
       }
     };
     auto x_store = [&](const XBatch& xb) {
 #pragma unroll
-      for (int j = 0; j < kXB; ++j) xs4[xb.at[j]] = xb.v[j];
+      for (int j = 0; j < kXB; ++j) xsw[xb.at[j]] = xb.v[j];
     };
     // the rest of the pass after its first batch: further batches, the
-    // floats past the last whole float4, and the zeroed run
+    // elements past the last whole word, and the zeroed run
     auto x_finish = [&](int pass) {
       const T* Xp = X + (int64_t)NB * pass * F;
-      const int rows = x_rows(pass), n4 = rows * F / 4;
-      for (int base = kThreads * kXB; base < n4; base += kThreads * kXB) {
+      const int rows = x_rows(pass), nw = rows * F / EPW;
+      for (int base = kThreads * kXB; base < nw; base += kThreads * kXB) {
         XBatch xb;
         x_load(xb, pass, base);
         x_store(xb);
       }
-      for (int e = 4 * n4 + tid; e < rows * F; e += kThreads) xs[e] = load_elem(Xp, e);
-      for (int e = tid; e < 16 * MS; e += kThreads) xs[rows * F + e] = 0.0f;
+      if constexpr (N16) {
+        unsigned short* xh = reinterpret_cast<unsigned short*>(xs);
+        const unsigned short* Xh = reinterpret_cast<const unsigned short*>(Xp);
+        for (int e = EPW * nw + tid; e < rows * F; e += kThreads) xh[e] = Xh[e];
+        for (int e = tid; e < ZRUN; e += kThreads) xh[rows * F + e] = 0;
+      } else {
+        for (int e = EPW * nw + tid; e < rows * F; e += kThreads) xs[e] = load_elem(Xp, e);
+        for (int e = tid; e < ZRUN; e += kThreads) xs[rows * F + e] = 0.0f;
+      }
     };
     {
       XBatch xb;
@@ -389,10 +449,8 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
 }
 
 // Writes the fragment section: out[((blk*4 + w)*(MS/4) + g)*64 + l][e] =
-// B[4*MS*w + MS*(l/16) + 4g + e][16 blk + l%16], zero past F or D (fp32; a
-// bf16 B widened exactly).
-template <typename T>
-__global__ __launch_bounds__(256) void pack_frag_kernel(const T* __restrict__ B,
+// B[4*MS*w + MS*(l/16) + 4g + e][16 blk + l%16], zero past F or D (fp32).
+__global__ __launch_bounds__(256) void pack_frag_kernel(const float* __restrict__ B,
                                                         float* __restrict__ out, int64_t F,
                                                         int64_t D, int64_t nblk, int MS) {
   const int64_t per_blk = (int64_t)256 * MS;  // 16 columns x 16*MS rows
@@ -404,6 +462,31 @@ __global__ __launch_bounds__(256) void pack_frag_kernel(const T* __restrict__ B,
     const int64_t f = 4 * MS * w + MS * (l / 16) + 4 * g + e;
     const int64_t col = blk * kW + l % 16;
     out[i] = (f < F && col < D) ? load_elem(B, f * D + col) : 0.0f;
+  }
+}
+
+// Writes the bf16 fragment section: word ((blk*4 + w)*S16 + s)*64 + l holds
+// the eight bf16 B[f][16 blk + l%16], f = 4*MS*w + 32*s + 8*(l/16) + 0..7,
+// zero where that row is past the wave's 4*MS rows, past F or past D.
+__global__ __launch_bounds__(256) void pack_frag16_kernel(const bf16raw* __restrict__ B,
+                                                          uint4* __restrict__ out, int64_t F,
+                                                          int64_t D, int64_t nblk, int MS) {
+  const int S16 = (MS + 7) / 8;
+  const int64_t per_blk = (int64_t)4 * S16 * 64;  // words per 16-column block
+  const int64_t total = nblk * per_blk;
+  const unsigned short* Bh = reinterpret_cast<const unsigned short*>(B);
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * 256) {
+    const int64_t l = i % 64, s = (i / 64) % S16, w = (i / (64 * S16)) % 4, blk = i / per_blk;
+    const int64_t col = blk * kW + l % 16;
+    uint32_t h[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t r = 32 * s + 8 * (l / 16) + j;  // row within the wave's share
+      const int64_t f = 4 * MS * w + r;
+      h[j] = (r < 4 * MS && f < F && col < D) ? Bh[f * D + col] : 0u;
+    }
+    out[i] = make_uint4(h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16);
   }
 }
 
@@ -468,14 +551,16 @@ hipError_t launch_frag_family(SmallPlan& p, const Args& a, const void* frag, int
 
 hipError_t launch_pack_frag(const void* B, void* out, int64_t F, int64_t D, int64_t nblk, int ms,
                             int dt, hipStream_t stream) {
+  if (dt == 1) {
+    const int64_t g16 = cdiv(nblk * 4 * ((ms + 7) / 8) * 64, 256);
+    hipLaunchKernelGGL(pack_frag16_kernel, dim3((unsigned)(g16 < 65536 ? g16 : 65536)), dim3(256),
+                       0, stream, (const bf16raw*)B, static_cast<uint4*>(out), F, D, nblk, ms);
+    return hipGetLastError();
+  }
   const int64_t g = cdiv(nblk * 256 * ms, 256);
   const dim3 grid((unsigned)(g < 65536 ? g : 65536));
-  if (dt == 0)
-    hipLaunchKernelGGL(pack_frag_kernel<float>, grid, dim3(256), 0, stream, (const float*)B,
-                       static_cast<float*>(out), F, D, nblk, ms);
-  else
-    hipLaunchKernelGGL(pack_frag_kernel<bf16raw>, grid, dim3(256), 0, stream,
-                       (const bf16raw*)B, static_cast<float*>(out), F, D, nblk, ms);
+  hipLaunchKernelGGL(pack_frag_kernel, grid, dim3(256), 0, stream, (const float*)B,
+                     static_cast<float*>(out), F, D, nblk, ms);
   return hipGetLastError();
 }
 
