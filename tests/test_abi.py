@@ -241,5 +241,12 @@ def test_routes_of_new_paths(L):
     assert b(4096, 784, 10240, 129, hd.HD_F32, 1) == b""      # packed path: K <= 128
     assert b(4096, 784, 10240, 512, hd.HD_F32, 0) == b"bundle_valu_kernel"
     assert b(4096, 784, 10240, 513, hd.HD_F32, 0) == b""
-    # the packed image of a bf16 model carries an fp32 fragment section
-    assert L.hd_model_packed_bytes(561, 10240, 6, hd.HD_BF16) >= 576 * 10240 * 4
+    # a packed image holds the large-batch fragments, the small-batch column
+    # tiles and the small-batch fragments: fp32 ones (MS = 36 rows per lane,
+    # 16*MS rows per column) for an fp32 model, bf16 ones (5 steps of 32 rows
+    # per wave) for a bf16 model
+    f32 = L.hd_model_packed_bytes(561, 10240, 6, hd.HD_F32)
+    b16 = L.hd_model_packed_bytes(561, 10240, 6, hd.HD_BF16)
+    assert f32 >= 2 * 561 * 10240 * 4 + 576 * 10240 * 4
+    assert b16 >= 2 * 561 * 10240 * 2 + 4 * 5 * 32 * 10240 * 2
+    assert b16 < f32 // 2 + 4 * 5 * 32 * 10240 * 2
