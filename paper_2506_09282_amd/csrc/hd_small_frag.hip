@@ -268,18 +268,20 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
       int at[kXB];
     };
     auto x_rows = [&](int pass) { return min(NB, N - NB * pass); };
-    // loads of one batch of the pass's words (base: first word index)
+    // loads of one batch of the pass's words (base: first word index). A
+    // pass has at least one word: the first has more than 8 rows of F >= 4,
+    // and a second pass is planned only for rows too long for one pass.
     auto x_load = [&](XBatch& xb, int pass, int base) {
       const T* Xp = X + (int64_t)NB * pass * F;
       const int nw = x_rows(pass) * F / EPW;
-      const int rot = nw > 0 ? (int)(((int64_t)blockIdx.x * 37 * 64) % nw) : 0;
+      const int rot = (int)(((int64_t)blockIdx.x * 37 * 64) % nw);
 #pragma unroll
       for (int j = 0; j < kXB; ++j) {
         const int i = base + j * kThreads + tid;
         const int r = i + rot >= nw ? i + rot - nw : i + rot;
         xb.at[j] = i < nw ? r : spare;
         if constexpr (N16)
-          xb.v[j] = reinterpret_cast<const uint4*>(Xp)[i < nw ? r : 0];
+          xb.v[j] = reinterpret_cast<const uint4*>(Xp)[i < nw ? r : rot];
         else
           xb.v[j] = load4w(Xp, i < nw ? r : rot);
       }
