@@ -229,6 +229,7 @@ INTEGER = [
     (32, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),
     (16, 561, 10240, 6, "bf16", True, "small_frag_mfma_kernel"),
     (40, 301, 1000, 16, "bf16", True, "small_frag_mfma_kernel"),
+    (60, 1000, 1500, 5, "bf16", True, "small_frag_mfma_kernel"),  # two sample passes
     (32, 561, 2048, 17, "bf16", True, "large_fused_kernel"),
     (128, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),  # two 64-sample calls
     (4, 561, 2048, 6, "bf16", True, "small_flat_kernel"),
@@ -425,7 +426,9 @@ PACKED_SMALL = [(1, 561, 10240, 6, "f32"), (3, 20, 1000, 4, "f32"), (8, 1100, 77
                 (64, 561, 10240, 6, "f32"), (37, 900, 8000, 11, "f32"),
                 (64, 561, 10240, 6, "bf16"), (45, 700, 3000, 16, "bf16"),
                 # 64-sample calls of a packed bf16 model up to 128 samples
-                (100, 561, 4096, 6, "bf16"), (65, 300, 2000, 10, "bf16")]
+                (100, 561, 4096, 6, "bf16"), (65, 300, 2000, 10, "bf16"),
+                # bf16 rows long enough for two sample passes
+                (64, 1000, 2000, 6, "bf16")]
 
 
 @pytest.mark.parametrize("N,F,D,K,dtype", PACKED_SMALL)
