@@ -47,7 +47,15 @@ constexpr int64_t kChunkedMaxN = 256;
 constexpr int64_t kChunkedMaxNBf16 = 128;  // a packed bf16 model's fragment kernel
 
 Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
-  if (dt == HD_I8) return hd::large_supported(N, F, D, K, dt) ? Route::kLarge : Route::kNone;
+  if (dt == HD_I8) {
+    // int8 on a packed model: the fragment kernel for small batches (it takes
+    // 16-byte aligned X; others fall back to the large-batch kernels, which
+    // the workspace query covers as well)
+    // (the large-batch bounds on F and D keep every sum exact)
+    if (!hd::large_supported(N, F, D, K, dt)) return Route::kNone;
+    if (tiled && N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt)) return Route::kSmall;
+    return Route::kLarge;
+  }
   const bool small_ok = N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt);
   if (small_ok && (dt == HD_F32 || N <= kSmallMaxNBf16)) return Route::kSmall;
   // a packed bf16 model carries fp32 fragments: the fragment kernel serves it
@@ -80,7 +88,7 @@ struct Image {
 Image image_layout(int64_t F, int64_t D, int64_t K, int dt) {
   Image im;
   im.large = align256(hd::large_packed_bytes(F, D, K, dt));
-  im.small = dt == HD_I8 ? 0 : align256(hd::small_packed_bytes(F, D, K, dt));
+  im.small = align256(hd::small_packed_bytes(F, D, K, dt));
   im.total = im.large + im.small;
   return im;
 }
@@ -161,6 +169,12 @@ size_t hd_model_packed_bytes(int64_t F, int64_t D, int64_t K, hd_dtype dt) {
 static size_t workspace_need(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool packed,
                              bool det) {
   const Route r = route(N, F, D, K, dt, packed);
+  if (r == Route::kSmall && dt == HD_I8) {
+    // an unaligned X takes the large-batch kernels instead
+    const size_t s = hd::small_workspace_bytes(N, F, D, K, dt, det);
+    const size_t l = hd::large_workspace_bytes(N, F, D, K, dt);
+    return s > l ? s : l;
+  }
   if (r == Route::kSmall || r == Route::kSmallChunked)
     return hd::small_workspace_bytes(small_n(r, N), F, D, K, dt, det);
   if (packed) return hd::large_workspace_bytes(N, F, D, K, dt);
@@ -214,8 +228,9 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
   if (!aligned(X, es) || !aligned(labels, 4) || !aligned(scores, 4) || !aligned(workspace, 256) ||
       (packed ? !aligned(packed, 256) : (!aligned(B, es) || !aligned(C, es))))
     return HD_ERR_ARG;
-  const Route r = route(N, F, D, K, dt, packed != nullptr);
+  Route r = route(N, F, D, K, dt, packed != nullptr);
   if (r == Route::kNone) return HD_ERR_UNSUPPORTED;
+  if (r == Route::kSmall && dt == HD_I8 && (uintptr_t)X % 16 != 0) r = Route::kLarge;
   const size_t need = workspace_need(N, F, D, K, dt, packed != nullptr, det);
   if (need > 0 && !workspace) return HD_ERR_ARG;
   if (workspace_bytes < need) return HD_ERR_WORKSPACE;

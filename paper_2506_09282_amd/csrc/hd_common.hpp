@@ -20,11 +20,12 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
 }
 
-// Element loads widened to fp32 (exact for both storage types).
+// Element loads widened to fp32 (exact for every storage type).
 __device__ __forceinline__ float load_elem(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float load_elem(const bf16raw* p, int64_t i) {
   return bf16_to_f32(p[i]);
 }
+__device__ __forceinline__ float load_elem(const int8_t* p, int64_t i) { return (float)p[i]; }
 
 // Four consecutive elements starting at p[i]; i must be a multiple of 4 and
 // the base 16-byte (fp32) / 8-byte (bf16) aligned.

@@ -77,10 +77,11 @@ int frag_ms(int64_t F) {
 }
 
 size_t frag_bytes(int64_t F, int64_t D, int dt) {
-  // fp32: MS/4 float4 per lane, wave and block; bf16: ceil(MS/8) words of
-  // eight bf16 (the bf16 matrix instruction's operands)
-  const int ms = dt <= 1 ? frag_ms(F) : 0;
-  if (dt == 1) return (size_t)cdiv(D, kW) * 4 * ((ms + 7) / 8) * 64 * 16;
+  // fp32: MS/4 float4 per lane, wave and block; bf16 and int8: ceil(MS/8)
+  // words of eight elements (16 or 8 bytes, the narrow matrix instructions'
+  // operands)
+  const int ms = frag_ms(F);
+  if (dt >= 1) return (size_t)cdiv(D, kW) * 4 * ((ms + 7) / 8) * 64 * (dt == 1 ? 16 : 8);
   return (size_t)cdiv(D, kW) * 256 * ms * sizeof(float);
 }
 
@@ -95,7 +96,8 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay
   if (v.nb == 0) return v;
   SmallPlan p{};
   p.nblocks = v.nblocks;
-  if (lay == kTiled && dt <= 1 && x_aligned && N > 8 && frag_ms(F) > 0) {
+  // int8 runs only on the fragment kernel, for every N
+  if (lay == kTiled && x_aligned && (N > 8 || dt == 2) && frag_ms(F) > 0) {
     const int ms = frag_ms(F);
     int64_t cslots = 1;  // the most blocks any workgroup walks
     for (int b = 0; b < v.grid; ++b) {
@@ -103,11 +105,12 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay
       cslots = c > cslots ? c : cslots;
     }
     // LDS: scores of every sample, the partials, the blocks' C, one pass's X
-    // (fp32: NB*F + 16*MS floats and a spare float4; bf16: NB*F + 32*MS
-    // bf16 and a spare word)
+    // (fp32: NB*F + 16*MS floats and a spare float4; bf16, int8: NB*F + 32*MS
+    // elements and a spare 16-byte word)
     auto frag_floats = [&](int64_t nti, int64_t npass) {
       const int64_t nbk = 16 * nti;
-      const int64_t xf = dt == 1 ? ((nbk * F + 32 * ms + 7) / 8 + 1) * 4
+      const int64_t epw = dt == 1 ? 8 : 16;
+      const int64_t xf = dt >= 1 ? ((nbk * F + 32 * ms + epw - 1) / epw + 1) * 4
                                  : (nbk * F + 16 * ms + 3) / 4 * 4 + 4;
       return (npass * nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 + cslots * K * kW + xf;
     };
@@ -202,15 +205,18 @@ __global__ __launch_bounds__(256) void pack_small_kernel(const T* __restrict__ s
   }
 }
 
-template <typename T>
+// WITH_B: the column tiles of B as well (not for int8)
+template <typename T, bool WITH_B>
 hipError_t pack_small_t(const void* B, const void* C, int64_t F, int64_t D, int64_t K,
                         void* out, hipStream_t stream) {
   const int64_t nblk = cdiv(D, kW);
   T* b = static_cast<T*>(out);
-  T* c = reinterpret_cast<T*>(static_cast<char*>(out) + (nblk * F * kW * sizeof(T) + 255) / 256 * 256);
+  T* c = reinterpret_cast<T*>(static_cast<char*>(out) +
+                              (WITH_B ? (nblk * F * kW * sizeof(T) + 255) / 256 * 256 : 0));
   const int64_t gb = cdiv(nblk * F * kW, 256), gc = cdiv(nblk * K * kW, 256);
-  hipLaunchKernelGGL(pack_small_kernel<T>, dim3((unsigned)(gb < 65536 ? gb : 65536)), dim3(256), 0,
-                     stream, (const T*)B, b, F, D, nblk);
+  if constexpr (WITH_B)
+    hipLaunchKernelGGL(pack_small_kernel<T>, dim3((unsigned)(gb < 65536 ? gb : 65536)), dim3(256),
+                       0, stream, (const T*)B, b, F, D, nblk);
   if (!C) {
     // no codebook yet (a model packed for training): class tiles are zero
     const hipError_t e = hipGetLastError();
@@ -260,6 +266,7 @@ static SmallPlan plan_stream(int64_t N, int64_t F, int64_t D, int64_t K, int dt)
 }
 
 bool small_supported(int64_t N, int64_t F, int64_t D, int64_t K, int dt) {
+  if (dt == 2) return plan_small(N, F, D, K, dt, kTiled, true).frag;  // packed int8 only
   return plan_valu(N, F, D, K, 8).nb > 0;
 }
 
@@ -282,13 +289,17 @@ const char* small_kernel_name(int64_t N, int64_t F, int64_t D, int64_t K, int dt
                                       : p.mfma  ? "small_mfma_kernel" : "small_valu_kernel";
 }
 
-// Small-batch section of a packed model: column tiles of B, column tiles of
-// C, then (fp32, 4 <= F <= 1024) the fragment copy of B, each on a 256-byte
-// boundary.
-size_t small_tiles_bytes(int64_t F, int64_t D, int64_t K, int dt) {
+// Small-batch section of a packed model: column tiles of B (not for int8,
+// which only the fragment kernel serves), column tiles of C, then
+// (4 <= F <= 1024) the fragment copy of B, each on a 256-byte boundary.
+size_t small_btiles_bytes(int64_t F, int64_t D, int dt) {
   const size_t es = dt == 0 ? 4 : 2;
+  return dt == 2 ? 0 : ((size_t)cdiv(D, kW) * F * kW * es + 255) / 256 * 256;
+}
+size_t small_tiles_bytes(int64_t F, int64_t D, int64_t K, int dt) {
+  const size_t es = dt == 0 ? 4 : dt == 1 ? 2 : 1;
   const size_t nblk = (size_t)cdiv(D, kW);
-  return (nblk * F * kW * es + 255) / 256 * 256 + (nblk * K * kW * es + 255) / 256 * 256;
+  return small_btiles_bytes(F, D, dt) + (nblk * K * kW * es + 255) / 256 * 256;
 }
 
 size_t small_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {
@@ -297,8 +308,9 @@ size_t small_packed_bytes(int64_t F, int64_t D, int64_t K, int dt) {
 
 hipError_t launch_pack_small(const void* B, const void* C, int64_t F, int64_t D, int64_t K, int dt,
                              void* out, hipStream_t stream) {
-  const hipError_t e = dt == 0 ? pack_small_t<float>(B, C, F, D, K, out, stream)
-                               : pack_small_t<bf16raw>(B, C, F, D, K, out, stream);
+  const hipError_t e = dt == 0   ? pack_small_t<float, true>(B, C, F, D, K, out, stream)
+                       : dt == 1 ? pack_small_t<bf16raw, true>(B, C, F, D, K, out, stream)
+                                 : pack_small_t<int8_t, false>(B, C, F, D, K, out, stream);
   if (e != hipSuccess || frag_bytes(F, D, dt) == 0) return e;
   return launch_pack_frag(B, static_cast<char*>(out) + small_tiles_bytes(F, D, K, dt), F, D,
                           cdiv(D, kW), frag_ms(F), dt, stream);
@@ -334,8 +346,7 @@ hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled,
   const void* frag = nullptr;
   if (tiled) {
     // the packed image's small-batch section
-    const size_t es = dt == 0 ? 4 : 2;
-    C = static_cast<const char*>(B) + (cdiv(D, kW) * F * kW * es + 255) / 256 * 256;
+    C = static_cast<const char*>(B) + small_btiles_bytes(F, D, dt);
     if (frag_bytes(F, D, dt) > 0) frag = static_cast<const char*>(B) + small_tiles_bytes(F, D, K, dt);
   } else {
     const bool vec = (D % 4 == 0) && ((uintptr_t)B % align == 0) && ((uintptr_t)C % align == 0);
@@ -349,6 +360,7 @@ hipError_t launch_small(const void* X, const void* B, const void* C, bool tiled,
     if (!frag) return hipErrorInvalidValue;
     return launch_frag_family(p, a, frag, dt);
   }
+  if (dt == 2) return hipErrorInvalidValue;  // int8: the fragment kernel only
   return launch_plan(p, a, dt, lay);
 }
 

@@ -27,6 +27,11 @@ namespace {
 //     from aligned dwords. The matrix instruction's k index is the same
 //     row of both operands, and its 16x16 result has the fp32 instruction's
 //     layout, so everything after the matrix steps is shared.
+//   int8: the same steps on v_mfma_i32_16x16x32_i8, eight int8 rows per lane
+//     and step in an 8-byte word (see pack_frag8_kernel); X is staged as
+//     int8. The int32 results are exact and convert exactly to fp32 while
+//     |V| <= 2^24 (F <= 1024 rows of products of at most 2^14), and the
+//     finish work then adds integers below 2^24, so the int8 path is exact.
 //
 // Persistent, one 512-thread workgroup per CU walking its column blocks,
 // with the waves split by role so that memory, matrix and reduction work
@@ -45,12 +50,12 @@ namespace {
 //      cslots >= blocks per workgroup
 // ---------------------------------------------------------------------------
 
-// One block's A operands per lane: MS/4 float4 (fp32) or ceil(MS/8) uint4
-// (eight bf16 each).
-template <int MS, bool N16>
+// One block's A operands per lane: MS/4 float4 (fp32), or ceil(MS/8) words
+// of eight elements (uint4 of bf16, uint2 of int8).
+template <int MS, int ESZ>
 struct FragBuf {
-  using Word = std::conditional_t<N16, uint4, float4>;
-  Word a[N16 ? (MS + 7) / 8 : MS / 4];
+  using Word = std::conditional_t<ESZ == 4, float4, std::conditional_t<ESZ == 2, uint4, uint2>>;
+  Word a[ESZ == 4 ? MS / 4 : (MS + 7) / 8];
 };
 
 // Four consecutive elements starting at element 4*i (16-byte or 8-byte aligned), as fp32.
@@ -62,6 +67,11 @@ __device__ __forceinline__ float4 load4w(const bf16raw* p, int64_t i) {
   return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
 }
+__device__ __forceinline__ float4 load4w(const int8_t* p, int64_t i) {
+  const uint32_t u = reinterpret_cast<const uint32_t*>(p)[i];
+  return make_float4((float)(int8_t)(u & 0xff), (float)(int8_t)((u >> 8) & 0xff),
+                     (float)(int8_t)((u >> 16) & 0xff), (float)(int8_t)(u >> 24));
+}
 
 template <typename T, int NTI, int MS, bool RING, int NPASS>
 __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
@@ -69,15 +79,20 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     int32_t* __restrict__ labels, float* __restrict__ scores, int N, int F, int D, int K, int act,
     int nblocks, int cslots, int lds_floats, void* __restrict__ workspace) {
   static_assert(NPASS == 1 || !RING, "two sample passes keep every block of B in registers");
-  constexpr bool N16 = std::is_same_v<T, bf16raw>;  // bf16 operands
+  constexpr int ESZ = (int)sizeof(T);
+  constexpr bool N16 = ESZ == 2;  // bf16 operands
+  constexpr bool N8 = ESZ == 1;   // int8 operands
+  constexpr bool NARROW = ESZ < 4;  // 32-row steps of eight elements per lane
   constexpr int NB = 16 * NTI;  // samples per pass
   constexpr int G4 = MS / 4;
   constexpr int S16 = (MS + 7) / 8;
-  constexpr int NW = N16 ? S16 : G4;  // 16-byte A operand words per lane per block
+  constexpr int NW = NARROW ? S16 : G4;  // A operand words per lane per block
   // X operands: they do not depend on the block, so when the registers allow
   // they are read from LDS once per pass into registers (no LDS latency
   // between matrix instructions)
-  constexpr bool kXReg = N16 ? 12 * S16 + 4 * S16 * NTI <= 180 : 3 * MS + NTI * MS <= 180;
+  // (registers: three B buffers and NTI X words of NW words each)
+  constexpr int kWordRegs = ESZ == 1 ? 2 : 4;
+  constexpr bool kXReg = (3 + NTI) * NW * kWordRegs <= 180;
   extern __shared__ __attribute__((aligned(16))) float smem[];
   float* sl = smem;                                  // [NPASS*NB*K]
   float* red = sl + (NPASS * NB * K + 3) / 4 * 4;    // [2][4][NTI][16][16]
@@ -103,7 +118,7 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     // B fragments of blocks 0, 1, 2. Blocks past the workgroup's last one
     // are "loaded" from a single broadcast address (one 16-byte request per
     // wave instruction), so the load count per step never depends on a branch.
-    using Buf = FragBuf<MS, N16>;
+    using Buf = FragBuf<MS, ESZ>;
     using Word = typename Buf::Word;
     const Word* Bw = reinterpret_cast<const Word*>(Bf);
     Buf b0, b1, b2;
@@ -118,10 +133,10 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     __syncthreads();  // competes with one block of B only; X and C are in LDS
     load_b(b1, 1);
 
-    // fp32: this lane's X^T rows start at xoff; bf16: its eight X values of
-    // step s, tile t start at element xoff + 16*t*F + 32*s
-    const int xoff = N16 ? (lane & 15) * F + 4 * MS * cw + 8 * (lane >> 4)
-                         : (lane & 15) * F + 4 * MS * cw + MS * (lane >> 4);
+    // fp32: this lane's X^T rows start at xoff; bf16, int8: its eight X
+    // values of step s, tile t start at element xoff + 16*t*F + 32*s
+    const int xoff = NARROW ? (lane & 15) * F + 4 * MS * cw + 8 * (lane >> 4)
+                            : (lane & 15) * F + 4 * MS * cw + MS * (lane >> 4);
     // eight consecutive bf16 X values from element e: the five dwords that
     // hold elements e - e % 2 .. e + 9, realigned by 0 or 2 bytes
     auto x16 = [&](int e) {
@@ -131,11 +146,21 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
       return make_uint4(__builtin_amdgcn_alignbyte(w1, w0, sh), __builtin_amdgcn_alignbyte(w2, w1, sh),
                         __builtin_amdgcn_alignbyte(w3, w2, sh), __builtin_amdgcn_alignbyte(w4, w3, sh));
     };
-    using XWord = std::conditional_t<N16, uint4, float4>;
+    // eight consecutive int8 X values from element e: three aligned dwords
+    // realigned by 0..3 bytes
+    auto x8 = [&](int e) {
+      const uint32_t* q = reinterpret_cast<const uint32_t*>(xs) + (e >> 2);
+      const uint32_t w0 = q[0], w1 = q[1], w2 = q[2];
+      const uint32_t sh = (uint32_t)(e & 3);
+      return make_uint2(__builtin_amdgcn_alignbyte(w1, w0, sh), __builtin_amdgcn_alignbyte(w2, w1, sh));
+    };
+    using XWord = typename Buf::Word;
     XWord xr[kXReg ? NW : 1][kXReg ? NTI : 1];
     auto x_word = [&](int g, int t) -> XWord {
       if constexpr (N16) {
         return x16(xoff + 16 * t * F + 32 * g);
+      } else if constexpr (N8) {
+        return x8(xoff + 16 * t * F + 32 * g);
       } else {
         const float* q = xs + xoff + 16 * t * F + 4 * g;
         return make_float4(q[0], q[1], q[2], q[3]);
@@ -153,11 +178,12 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     load_b(b2, 2);
     auto multiply = [&](const Buf& x, int i) {
       // two independent accumulator chains per sample tile, interleaved over
-      // the tiles (fp32: steps 4g, 4g+2 and 4g+1, 4g+3; bf16: even and odd
-      // 32-row steps)
-      f32x4 acc[NTI][2];
+      // the tiles (fp32: steps 4g, 4g+2 and 4g+1, 4g+3; bf16, int8: even and
+      // odd 32-row steps)
+      using Acc = std::conditional_t<N8, i32x4, f32x4>;
+      Acc acc[NTI][2];
 #pragma unroll
-      for (int t = 0; t < NTI; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int t = 0; t < NTI; ++t) acc[t][0] = acc[t][1] = Acc{0, 0, 0, 0};
 #pragma unroll
       for (int g = 0; g < NW; ++g) {
         XWord xg[NTI];
@@ -174,6 +200,12 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
           for (int t = 0; t < NTI; ++t)
             acc[t][g & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 __builtin_bit_cast(bf16x8, x.a[g]), __builtin_bit_cast(bf16x8, xg[t]),
+                acc[t][g & 1], 0, 0, 0);
+        } else if constexpr (N8) {
+#pragma unroll
+          for (int t = 0; t < NTI; ++t)
+            acc[t][g & 1] = __builtin_amdgcn_mfma_i32_16x16x32_i8(
+                __builtin_bit_cast(long, x.a[g]), __builtin_bit_cast(long, xg[t]),
                 acc[t][g & 1], 0, 0, 0);
         } else {
 #pragma unroll
@@ -196,8 +228,10 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
                   (lane & 15) * 4 + (lane >> 4);
 #pragma unroll
       for (int t = 0; t < NTI; ++t)
-        r[t * 64] = make_float4(acc[t][0][0] + acc[t][1][0], acc[t][0][1] + acc[t][1][1],
-                                acc[t][0][2] + acc[t][1][2], acc[t][0][3] + acc[t][1][3]);
+        r[t * 64] = make_float4((float)(acc[t][0][0] + acc[t][1][0]),
+                                (float)(acc[t][0][1] + acc[t][1][1]),
+                                (float)(acc[t][0][2] + acc[t][1][2]),
+                                (float)(acc[t][0][3] + acc[t][1][3]));
     };
     // Step i (one barrier each): multiply block i and reload its buffer with
     // block i+3. B buffers are named per step (no register copies, which
@@ -253,11 +287,11 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     // read the next row (finite values times zero B) or, after the last row,
     // the zeroed run of 16*MS floats. Rows of a pass start 16-byte aligned
     // (NB*F floats per pass, NB a multiple of 16).
-    // X moves in 16-byte words: four fp32 or eight bf16 elements (bf16 X is
-    // staged as it is, fp32 the same)
-    using SWord = std::conditional_t<N16, uint4, float4>;
-    constexpr int EPW = N16 ? 8 : 4;    // elements per word
-    constexpr int ZRUN = N16 ? 32 * MS : 16 * MS;  // zeroed elements after the rows
+    // X moves in 16-byte words of 16 / ESZ elements, staged as it is
+    // (a native vector type: HIP's uint4 copied as a whole goes through the stack)
+    using SWord = std::conditional_t<NARROW, i32x4, float4>;
+    constexpr int EPW = 16 / ESZ;  // elements per word
+    constexpr int ZRUN = NARROW ? 32 * MS : 16 * MS;  // zeroed elements after the rows
     // words per thread for NB rows of up to 16*MS elements: NB*16*MS / (EPW * 256)
     constexpr int kXBw = (NTI * MS + EPW - 1) / EPW;
     constexpr int kXB = kXBw < 40 ? kXBw : 40;
@@ -280,8 +314,8 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
         const int i = base + j * kThreads + tid;
         const int r = i + rot >= nw ? i + rot - nw : i + rot;
         xb.at[j] = i < nw ? r : spare;
-        if constexpr (N16)
-          xb.v[j] = reinterpret_cast<const uint4*>(Xp)[i < nw ? r : rot];
+        if constexpr (NARROW)
+          xb.v[j] = reinterpret_cast<const i32x4*>(Xp)[i < nw ? r : rot];
         else
           xb.v[j] = load4w(Xp, i < nw ? r : rot);
       }
@@ -300,9 +334,10 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
         x_load(xb, pass, base);
         x_store(xb);
       }
-      if constexpr (N16) {
-        unsigned short* xh = reinterpret_cast<unsigned short*>(xs);
-        const unsigned short* Xh = reinterpret_cast<const unsigned short*>(Xp);
+      if constexpr (NARROW) {
+        using E = std::conditional_t<N16, unsigned short, unsigned char>;
+        E* xh = reinterpret_cast<E*>(xs);
+        const E* Xh = reinterpret_cast<const E*>(Xp);
         for (int e = EPW * nw + tid; e < rows * F; e += kThreads) xh[e] = Xh[e];
         for (int e = tid; e < ZRUN; e += kThreads) xh[rows * F + e] = 0;
       } else {
@@ -492,6 +527,32 @@ __global__ __launch_bounds__(256) void pack_frag16_kernel(const bf16raw* __restr
   }
 }
 
+// Writes the int8 fragment section: word ((blk*4 + w)*S16 + s)*64 + l holds
+// the eight int8 B[f][16 blk + l%16], f = 4*MS*w + 32*s + 8*(l/16) + 0..7,
+// zero where that row is past the wave's 4*MS rows, past F or past D.
+__global__ __launch_bounds__(256) void pack_frag8_kernel(const int8_t* __restrict__ B,
+                                                         uint2* __restrict__ out, int64_t F,
+                                                         int64_t D, int64_t nblk, int MS) {
+  const int S16 = (MS + 7) / 8;
+  const int64_t per_blk = (int64_t)4 * S16 * 64;  // words per 16-column block
+  const int64_t total = nblk * per_blk;
+  const uint8_t* Bb = reinterpret_cast<const uint8_t*>(B);
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * 256) {
+    const int64_t l = i % 64, s = (i / 64) % S16, w = (i / (64 * S16)) % 4, blk = i / per_blk;
+    const int64_t col = blk * kW + l % 16;
+    uint32_t b[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t r = 32 * s + 8 * (l / 16) + j;  // row within the wave's share
+      const int64_t f = 4 * MS * w + r;
+      b[j] = (r < 4 * MS && f < F && col < D) ? Bb[f * D + col] : 0u;
+    }
+    out[i] = make_uint2(b[0] | b[1] << 8 | b[2] << 16 | b[3] << 24,
+                        b[4] | b[5] << 8 | b[6] << 16 | b[7] << 24);
+  }
+}
+
 
 template <typename T, int NTI, int MS, bool RING, int NPASS>
 hipError_t launch_frag_t(const SmallPlan& p, const Args& a, const void* frag) {
@@ -548,15 +609,21 @@ hipError_t launch_frag_nti(const SmallPlan& p, const Args& a, const void* frag) 
 
 hipError_t launch_frag_family(SmallPlan& p, const Args& a, const void* frag, int dt) {
   widen_for_final(p, a.N, a.K);
+  if (dt == 2) return launch_frag_nti<int8_t>(p, a, frag);
   return dt == 0 ? launch_frag_nti<float>(p, a, frag) : launch_frag_nti<bf16raw>(p, a, frag);
 }
 
 hipError_t launch_pack_frag(const void* B, void* out, int64_t F, int64_t D, int64_t nblk, int ms,
                             int dt, hipStream_t stream) {
-  if (dt == 1) {
-    const int64_t g16 = cdiv(nblk * 4 * ((ms + 7) / 8) * 64, 256);
-    hipLaunchKernelGGL(pack_frag16_kernel, dim3((unsigned)(g16 < 65536 ? g16 : 65536)), dim3(256),
-                       0, stream, (const bf16raw*)B, static_cast<uint4*>(out), F, D, nblk, ms);
+  if (dt >= 1) {
+    const int64_t gn = cdiv(nblk * 4 * ((ms + 7) / 8) * 64, 256);
+    const dim3 g((unsigned)(gn < 65536 ? gn : 65536));
+    if (dt == 1)
+      hipLaunchKernelGGL(pack_frag16_kernel, g, dim3(256), 0, stream, (const bf16raw*)B,
+                         static_cast<uint4*>(out), F, D, nblk, ms);
+    else
+      hipLaunchKernelGGL(pack_frag8_kernel, g, dim3(256), 0, stream, (const int8_t*)B,
+                         static_cast<uint2*>(out), F, D, nblk, ms);
     return hipGetLastError();
   }
   const int64_t g = cdiv(nblk * 256 * ms, 256);

@@ -189,13 +189,21 @@ def test_packed_training_argument_errors(L):
 
 def test_int8_limits(L):
     """The int8 variant: HardSign only, exactness bounds on F and D, the
-    large-batch kernels for every batch size, no stage-alone or streaming call."""
+    fragment kernel for small batches on a packed model and the large-batch
+    kernels otherwise, no stage-alone or streaming call."""
     I8 = hd.HD_I8
     assert _infer(L, dt=I8, act=1) == hd.HD_ERR_UNSUPPORTED
     assert _infer(L, dt=I8, F=131072) == hd.HD_ERR_UNSUPPORTED
     assert _infer(L, dt=I8, D=131073) == hd.HD_ERR_UNSUPPORTED
     assert _infer(L, dt=I8, K=129) == hd.HD_ERR_UNSUPPORTED
-    assert L.hd_infer_kernel(1, 561, 10240, 6, I8, 1) == b"large_fused_kernel"
+    for n in (1, 9, 32, 64):
+        assert L.hd_infer_kernel(n, 561, 10240, 6, I8, 1) == b"small_frag_mfma_kernel"
+    assert L.hd_infer_kernel(65, 561, 10240, 6, I8, 1) == b"large_fused_kernel"
+    assert L.hd_infer_kernel(32, 561, 10240, 6, I8, 0) == b"large_fused_kernel"  # raw B, C
+    assert L.hd_infer_kernel(32, 1025, 10240, 6, I8, 1) != b"small_frag_mfma_kernel"
+    assert L.hd_infer_kernel(32, 561, 10240, 17, I8, 1) == b"large_fused_kernel"
+    # (an X that is not 16-byte aligned falls back to the large-batch kernels,
+    # and the workspace query covers that route: tests/test_gpu_int8.py)
     assert L.hd_infer_kernel(1, 131071, 64, 2, I8, 1) == b"large_chunked_kernel"
     assert L.hd_encode(FAKE, FAKE, FAKE, 4, 8, 16, I8, 0, None) == hd.HD_ERR_UNSUPPORTED
     assert L.hd_similarity(FAKE, FAKE, FAKE, None, 4, 16, 3, I8, None) == hd.HD_ERR_UNSUPPORTED
@@ -204,8 +212,16 @@ def test_int8_limits(L):
     assert L.hd_infer_stream_workspace_bytes(4, 1, 561, 10240, 6, I8) == 0
     assert L.hd_bundle_kernel(100, 617, 4096, 26, I8, 1) == b"bundle_mfma_kernel"
     assert L.hd_bundle_kernel(100, 617, 4096, 26, I8, 0) == b""
-    # the packed image has no small-batch section
+    # the packed image's small-batch section holds C's column tiles and the
+    # fragment copy of B (F <= 1024), not B's column tiles
     assert L.hd_model_packed_bytes(617, 4096, 26, I8) < L.hd_model_packed_bytes(617, 4096, 26, 1)
+    nblk, s16 = 4096 // 16, (48 + 7) // 8  # F = 617: 48 rows per lane
+    frag = nblk * 4 * s16 * 64 * 8
+    ctiles = -(-nblk * 26 * 16 // 256) * 256
+    assert L.hd_model_packed_bytes(617, 4096, 26, I8) >= frag + ctiles
+    # F = 1025 has no fragment copy (1 MB at F = 1024) and one more 32-row
+    # step of the large-batch section (128 KB)
+    assert L.hd_model_packed_bytes(1025, 4096, 26, I8) < L.hd_model_packed_bytes(1024, 4096, 26, I8)
 
 
 def test_deterministic_flag(L):

@@ -51,7 +51,7 @@ def check(y, S, ref):
 CASES = [
     (300, 617, 4096, 26, True, "large_fused_kernel"),
     (300, 617, 4096, 26, False, "large_fused_kernel"),
-    (1, 561, 10240, 6, True, "large_fused_kernel"),
+    (1, 561, 10240, 6, False, "large_fused_kernel"),
     (129, 300, 2000, 100, True, "large_fused_kernel"),
     (77, 1000, 999, 40, False, "large_fused_kernel"),
     (200, 3001, 1024, 10, True, "large_fused_kernel"),
@@ -71,6 +71,90 @@ def test_int8_bit_exact(hd, N, F, D, K, packed, kernel):
     X, B, C = hd_inputs.make_int8_inputs(N, F, D, K, seed=N + F + K)
     y, S = run(hd, X, B, C, packed)
     check(y, S, oracle.infer(X, B, C))
+
+
+# Small batches on a packed model: the fragment kernel on the int8 matrix
+# instructions (one to four 16-sample tiles, 12 to 64 rows per lane, the B
+# ring when a workgroup walks more than three column blocks, ragged D, the
+# smallest F, the most classes it takes).
+SMALL_CASES = [
+    (1, 561, 10240, 6),
+    (9, 617, 4096, 16),
+    (16, 33, 1000, 5),
+    (32, 561, 10240, 6),
+    (48, 700, 2000, 10),
+    (64, 1024, 3000, 16),
+    (64, 561, 20480, 6),
+    (24, 4, 64, 2),
+    (40, 1000, 13000, 5),
+    (63, 250, 777, 7),
+]
+
+
+@pytest.mark.parametrize("N,F,D,K", SMALL_CASES)
+@pytest.mark.parametrize("det", [False, True])
+def test_int8_small_bit_exact(hd, N, F, D, K, det):
+    torch = torch_or_skip()
+    assert hd.infer_kernel(N, F, D, K, torch.int8, packed=True) == "small_frag_mfma_kernel"
+    announce(f"int8 small N={N} F={F} D={D} K={K} det={det}")
+    X, B, C = hd_inputs.make_int8_inputs(N, F, D, K, seed=N + F + K)
+    model = hd.pack_model(i8(B), i8(C))
+    y, S = hd.infer_packed(i8(X), model, return_scores=True, deterministic=det)
+    torch.cuda.synchronize()
+    check(y.cpu().numpy(), S.cpu().numpy().astype(np.float64), oracle.infer(X, B, C))
+
+
+def test_int8_small_extreme_sums_and_ties(hd):
+    """F = 1024 with every product at +-128 * 128 (sums reach 2^24, still exact
+    in the int32 accumulators and in fp32), then X, B in {-1, 0, 1} with many
+    zero sums (HardSign +1) and tied classes (the lowest index wins)."""
+    torch = torch_or_skip()
+    N, F, D, K = 5, 1024, 256, 3
+    announce(f"int8 small extremes N={N} F={F}")
+    X = np.full((N, F), -128, np.int8)
+    X[1] = 127
+    X[2, ::2] = 127
+    X[3, 1::4] = 0
+    B = np.full((F, D), -128, np.int8)
+    B[:, 1::3] = 127
+    C = hd_inputs.make_int8_inputs(1, 1, D, K, seed=3)[2]
+    assert hd.infer_kernel(N, F, D, K, torch.int8, packed=True) == "small_frag_mfma_kernel"
+    ref = oracle.infer(X, B, C, want_va=True)
+    assert np.abs(ref["V"]).max() == 2 ** 24
+    y, S = run(hd, X, B, C, True)
+    check(y, S, ref)
+    N, F, D, K = 40, 300, 1000, 6
+    X, B, C = hd_inputs.make_int8_inputs(N, F, D, K, seed=9, lo=-1, hi=1)
+    C[3] = C[1]
+    C[5] = C[1]
+    ref = oracle.infer(X, B, C, want_va=True)
+    assert (ref["V"] == 0).sum() > 100
+    y, S = run(hd, X, B, C, True)
+    check(y, S, ref)
+
+
+def test_int8_small_unaligned_x_and_noalloc(hd):
+    """An X that does not start on a 16-byte boundary takes the large-batch
+    kernels within the queried workspace; the no-allocation entry point runs
+    the fragment kernel on the library's scratch."""
+    torch = torch_or_skip()
+    N, F, D, K = 32, 561, 10240, 6
+    announce(f"int8 small unaligned X and no-alloc N={N}")
+    X, B, C = hd_inputs.make_int8_inputs(N, F, D, K, seed=21)
+    model = hd.pack_model(i8(B), i8(C))
+    ref = oracle.infer(X, B, C)
+    buf = torch.zeros(N * F + 64, dtype=torch.int8, device="cuda")
+    Xu = buf[1:1 + N * F].view(N, F)
+    Xu.copy_(i8(X))
+    assert Xu.data_ptr() % 16 != 0
+    y, S = hd.infer_packed(Xu, model, return_scores=True)
+    torch.cuda.synchronize()
+    check(y.cpu().numpy(), S.cpu().numpy().astype(np.float64), ref)
+    for n in (N, 9):
+        y, S = hd.infer_packed_noalloc(i8(X[:n]), model, return_scores=True)
+        torch.cuda.synchronize()
+        r = oracle.infer(X[:n], B, C)
+        check(y.cpu().numpy(), S.cpu().numpy().astype(np.float64), r)
 
 
 @pytest.mark.parametrize("N,F,kernel", [(300, 40, "large_fused_kernel"),
