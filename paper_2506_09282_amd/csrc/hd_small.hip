@@ -104,25 +104,25 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay
       const int c = block_walk(b, v.grid, v.nblocks).count();
       cslots = c > cslots ? c : cslots;
     }
-    // LDS: scores of every sample, the partials, the blocks' C, one pass's X
-    // (fp32: NB*F + 16*MS floats and a spare float4; bf16, int8: NB*F + 32*MS
-    // elements and a spare 16-byte word)
-    auto frag_floats = [&](int64_t nti, int64_t npass) {
+    // LDS: the partials (later each finish wave's scores), the blocks' C,
+    // one pass's X (fp32: NB*F + 16*MS floats and a spare float4; bf16,
+    // int8: NB*F + 32*MS elements and a spare 16-byte word)
+    auto frag_floats = [&](int64_t nti) {
       const int64_t nbk = 16 * nti;
       const int64_t epw = dt == 1 ? 8 : 16;
       const int64_t xf = dt >= 1 ? ((nbk * F + 32 * ms + epw - 1) / epw + 1) * 4
                                  : (nbk * F + 16 * ms + 3) / 4 * 4 + 4;
-      return (npass * nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 + cslots * K * kW + xf;
+      return 2 * kWaves * nti * 256 + cslots * K * kW + xf;
     };
     // all samples in one pass; else, when X of all of them does not fit and
     // no workgroup walks more than three blocks (B stays in registers), two
     // passes of 32
     int64_t nti = cdiv(N, 16), npass = 1;
-    int64_t floats = frag_floats(nti, 1);
+    int64_t floats = frag_floats(nti);
     if ((int64_t)sizeof(float) * floats > kLdsBudget && N > 32 && cslots <= 3) {
       nti = 2;
       npass = 2;
-      floats = frag_floats(2, 2);
+      floats = frag_floats(2);
     }
     if (K <= kFragMaxK && (int64_t)sizeof(float) * floats <= kLdsBudget) {
       p.frag = true;

@@ -42,10 +42,10 @@ namespace {
 //   waves 0..3 (finish): first stage X and the C values of every block of
 //     the workgroup into LDS (their loads do not queue behind B, since load
 //     counters are per wave), then, while block i is multiplied, turn block
-//     i-1's partials into HardSign values and per-pair partial scores
-//     (Eq. 1, Eq. 8).
+//     i-1's partials into HardSign values (Eq. 1) and multiply them with
+//     the block's C on the fp32 matrix instruction (Eq. 8).
 // One barrier per block hands red from one role to the other.
-// LDS: sl[NPASS*NB*K] | red[2][4 waves][NTI][16 n][16 d] | cs[cslots][K*16] |
+// LDS: red[2][4 waves][NTI][4 q][64 lanes] | cs[cslots][K*16] |
 //      xs: fp32 [NB*F + 16*MS] (+ 4 spare), bf16 [NB*F + 32*MS] (+ 8 spare);
 //      cslots >= blocks per workgroup
 // ---------------------------------------------------------------------------
@@ -94,8 +94,7 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
   constexpr int kWordRegs = ESZ == 1 ? 2 : 4;
   constexpr bool kXReg = (3 + NTI) * NW * kWordRegs <= 180;
   extern __shared__ __attribute__((aligned(16))) float smem[];
-  float* sl = smem;                                  // [NPASS*NB*K]
-  float* red = sl + (NPASS * NB * K + 3) / 4 * 4;    // [2][4][NTI][16][16]
+  float* red = smem;                         // [2][4][NTI][4][64]
   float* cs = red + 2 * kWaves * NTI * 256;  // [cslots][K*16]: C of block i at slot i
   float* xs = cs + cslots * K * kW;          // X of one pass (fp32 or bf16)
   const SmallWs ws = small_ws(workspace);
@@ -108,6 +107,14 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
   act &= 1;
   const int R = det ? G : replicas(G, N * K);
   const int nmine = walk.count();
+  // A workgroup may own no block (when the blocks of an XCD are fewer than
+  // its workgroups). The two roles' barrier counts below assume at least one
+  // block, so such a workgroup only takes its ticket: it has nothing to add.
+  if (nmine == 0) {
+    publish_and_finish<kFragThreads>(smem, 0, 0, N, K, R, ws, labels, scores, smem, lds_floats,
+                                     true, det);
+    return;
+  }
 
   // The two roles run separate code paths from the first instruction, with
   // the same barrier count (nmine + 2), so that the compiler's load-counter
@@ -222,16 +229,13 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
             acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].w, xg[t].w, acc[t][1], 0, 0, 0);
         }
       }
-      // lane l holds V^T[d = 4(l/16) + q][n = l%16], q = 0..3: one 16-byte
-      // store into red[i % 2][cw][t][n][d]
-      float4* r = reinterpret_cast<float4*>(red + ((i & 1) * kWaves + cw) * NTI * 256) +
-                  (lane & 15) * 4 + (lane >> 4);
+      // lane l holds V^T[d = 4(l/16) + q][n = l%16], q = 0..3; value q goes
+      // to plane q of red[i % 2][cw][t], at position l (conflict-free)
+      float* r = red + ((i & 1) * kWaves + cw) * NTI * 256 + lane;
 #pragma unroll
       for (int t = 0; t < NTI; ++t)
-        r[t * 64] = make_float4((float)(acc[t][0][0] + acc[t][1][0]),
-                                (float)(acc[t][0][1] + acc[t][1][1]),
-                                (float)(acc[t][0][2] + acc[t][1][2]),
-                                (float)(acc[t][0][3] + acc[t][1][3]));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) r[t * 256 + q * 64] = (float)(acc[t][0][q] + acc[t][1][q]);
     };
     // Step i (one barrier each): multiply block i and reload its buffer with
     // block i+3. B buffers are named per step (no register copies, which
@@ -359,68 +363,34 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     }
     __syncthreads();
 
-    // Block i's partial scores (Eq. 1, Eq. 8). The four finish waves, one per
-    // SIMD, share the work: on this chip fp32 VALU instructions do not
-    // overlap the fp32 matrix instructions of their SIMD, so the finish work
-    // adds to the matrix time of whichever SIMDs run it. LPS lanes per sample
-    // n (256 / NB, at least 4), each with CPL = 16 / LPS consecutive columns:
-    // a lane sums the four wave partials of its V values, applies HardSign,
-    // and adds its CPL-term share of every class's inner product to its own
-    // running sum (classes in groups of four under a uniform branch, the
-    // group's C reads issued together; a class past K reads class K-1 and
-    // its sum is never used). The LPS shares are added once, after the last
-    // block. Columns past D need no mask: the packed C is zero there.
-    constexpr int LPS = NB <= 16 ? 16 : NB <= 32 ? 8 : 4;
-    constexpr int CPL = 16 / LPS;
-    const int fn = tid / LPS, fc = (tid % LPS) * CPL;
-    float psum[kFragMaxK];
+    // Block i's partial scores (Eq. 1, Eq. 8) on the fp32 matrix
+    // instruction. On this chip fp32 VALU instructions do not overlap the
+    // fp32 matrix instructions of their SIMD, so every finish instruction
+    // adds to the matrix time of its SIMD; one matrix instruction per tile
+    // replaces the per-class multiply-adds. Finish wave fw takes the
+    // columns d = 4j + fw (j = 0..3) of every tile: lane l sums the four
+    // wave partials of V^T[d = 4(l/16) + fw][n = l%16] (plane fw of red),
+    // applies HardSign, and feeds it as the B operand (k = l/16, column n)
+    // of S^T += C_blk · H^T, whose A operand is C[k = l%16][4(l/16) + fw]
+    // (rows past K repeat class K-1 and are never read). The result,
+    // S^T[4(l/16) + r][l%16], accumulates over the blocks; the four waves'
+    // sums are added once, at publication. Columns past D need no mask:
+    // the packed C is zero there.
+    const int fw = wave;
+    const float* cl = cs + min(lane & 15, K - 1) * kW + 4 * (lane >> 4) + fw;
+    f32x4 sacc[NPASS][NTI];
 #pragma unroll
-    for (int k = 0; k < kFragMaxK; ++k) psum[k] = 0.0f;
-    auto lds_vec = [](const float* p, float (&v)[CPL]) {
-      if constexpr (CPL == 4) {
-        const float4 t = *reinterpret_cast<const float4*>(p);
-        v[0] = t.x;
-        v[1] = t.y;
-        v[2] = t.z;
-        v[3] = t.w;
-      } else if constexpr (CPL == 2) {
-        const float2 t = *reinterpret_cast<const float2*>(p);
-        v[0] = t.x;
-        v[1] = t.y;
-      } else {
-        v[0] = *p;
-      }
-    };
-    auto finish = [&](int i, int nb) {
-      if (fn >= nb) return;  // a sample's lanes drop out together
-      // red[i % 2][w][t][n16][16 d]: sample fn = 16 t + n16 is row fn of wave w's part
-      const float* r = red + (i & 1) * kWaves * NTI * 256 + fn * 16 + fc;
-      float v[CPL];
-      lds_vec(r, v);
+    for (int p = 0; p < NPASS; ++p)
 #pragma unroll
-      for (int w = 1; w < kWaves; ++w) {
-        float u[CPL];
-        lds_vec(r + w * NTI * 256, u);
+      for (int t = 0; t < NTI; ++t) sacc[p][t] = f32x4{0, 0, 0, 0};
+    auto finish = [&](int i, f32x4 (&sa)[NTI]) {
+      const float cv = cl[i * K * kW];
+      const float* r = red + (i & 1) * kWaves * NTI * 256 + fw * 64 + lane;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) v[c] += u[c];
-      }
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) v[c] = activate(v[c], act);
-      const float* cb = cs + i * K * kW + fc;
-#pragma unroll
-      for (int kg = 0; kg < kFragMaxK / 4; ++kg) {
-        if (4 * kg < K) {
-          float cv[4][CPL];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int k = 4 * kg + j;
-            lds_vec(cb + (k < K ? k : K - 1) * kW, cv[j]);
-          }
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) psum[4 * kg + j] = fmaf(v[c], cv[j][c], psum[4 * kg + j]);
-        }
+      for (int t = 0; t < NTI; ++t) {
+        const float* q = r + t * 256;
+        const float v = (q[0] + q[NTI * 256]) + (q[2 * NTI * 256] + q[3 * NTI * 256]);
+        sa[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(cv, activate(v, act), sa[t], 0, 0, 0);
       }
     };
     // Step i (one barrier each, nmine + 1 steps per pass): finish block i-1
@@ -428,60 +398,48 @@ __global__ __launch_bounds__(kFragThreads, 1) void small_frag_mfma_kernel(
     // requested at the start of the first pass and stored once the compute
     // waves no longer read the first pass's X: after step 0 when they hold X
     // in registers, else after the pass.
-    auto dpp_add = [](float d, auto ctrl) {
-      return d + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                               0, __builtin_bit_cast(int, d), decltype(ctrl)::value,
-                                               0xf, 0xf, false));
-    };
-    using QuadSwap1 = std::integral_constant<int, 0xB1>;  // quad_perm [1,0,3,2]
-    using QuadSwap2 = std::integral_constant<int, 0x4E>;  // quad_perm [2,3,0,1]
-    using HalfMirror = std::integral_constant<int, 0x141>;  // row_half_mirror
-    using RowMirror = std::integral_constant<int, 0x140>;   // row_mirror
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
-      const int nb = x_rows(pass);
       XBatch next;
       const bool more = pass + 1 < NPASS;
       if (more) x_load(next, pass + 1, 0);
-      const bool early = more && kXReg && nmine >= 1;
+      const bool early = more && kXReg;
       for (int i = 0; i <= nmine; ++i) {
-        if (i > 0) finish(i - 1, nb);
+        if (i > 0) finish(i - 1, sacc[pass]);
         if (early && i == 1) x_store(next);
         __syncthreads();
       }
-      // The sample's LPS lanes are consecutive, aligned and drop out
-      // together. DPP sums them without LDS traffic: the two quad swaps leave
-      // each quad's total in its lanes, the half-row mirror (lane l of 8
-      // reads lane 7-l) adds the other quad of 8, the row mirror (l of 16
-      // reads 15-l) the other half-row; every lane then holds its sample's
-      // total.
-      if (fn < nb) {
-#pragma unroll
-        for (int kg = 0; kg < kFragMaxK / 4; ++kg) {
-          if (4 * kg < K) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int k = 4 * kg + j;
-              float d = dpp_add(dpp_add(psum[k], QuadSwap1{}), QuadSwap2{});
-              if constexpr (LPS >= 8) d = dpp_add(d, HalfMirror{});
-              if constexpr (LPS >= 16) d = dpp_add(d, RowMirror{});
-              if (k < K && tid % LPS == k % LPS) sl[(NB * pass + fn) * K + k] = d;
-            }
-          }
-        }
-      }
       if (more) {
-#pragma unroll
-        for (int k = 0; k < kFragMaxK; ++k) psum[k] = 0.0f;
         if (!early) x_store(next);
         x_finish(pass + 1);
         __syncthreads();  // the next pass's X is in LDS
       }
     }
+    // Each wave's sums, [fw][pass][t][lane][4], into red (no longer read by
+    // the compute waves after the last step's barrier).
+    f32x4* part = reinterpret_cast<f32x4*>(red) + fw * NPASS * NTI * 64 + lane;
+#pragma unroll
+    for (int p = 0; p < NPASS; ++p)
+#pragma unroll
+      for (int t = 0; t < NTI; ++t) part[(p * NTI + t) * 64] = sacc[p][t];
   }
   __syncthreads();
-  publish_and_finish<kFragThreads>(sl, 0, min(NPASS * NB, N), N, K, R, ws, labels, scores, smem,
-                                   lds_floats,
+  // The workgroup's partial scores: sample n = NB*p + 16t + j, class k is
+  // element k % 4 of lane 16(k/4) + j of each finish wave's tile (p, t),
+  // summed over the four waves in a fixed order.
+  {
+    float* my = ws.sacc + (int64_t)(blockIdx.x % R) * N * K;
+    const int rows = min(NPASS * NB, N);
+    const float* part = red;
+    for (int e = tid; e < rows * K; e += kFragThreads) {
+      const int n = e / K, k = e - n * K;
+      const int pt = n >> 4;  // pass * NTI + tile
+      const int o = (pt * 64 + (k >> 2) * 16 + (n & 15)) * 4 + (k & 3);
+      constexpr int WS = NPASS * NTI * 256;  // one wave's sums
+      publish_add(my + e, (part[o] + part[o + WS]) + (part[o + 2 * WS] + part[o + 3 * WS]));
+    }
+  }
+  publish_and_finish<kFragThreads>(smem, 0, 0, N, K, R, ws, labels, scores, smem, lds_floats,
                                    true, det);
 }
 
