@@ -29,22 +29,26 @@ bool det_of(int act) { return (act & HD_DETERMINISTIC) != 0; }
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 // Path choice. The split-D small-batch path serves small batches whenever its
-// scratch fits, everything else the batch-split matrix-core path, with two
+// scratch fits, everything else the batch-split matrix-core path, with these
 // exceptions taken from the measured samples/s curves (F = 561, D = 10240):
 // * bf16 above 8 samples with B as given: the small-batch VALU kernel makes
 //   several passes over B (40 us at N = 16, 72 us at N = 32), the matrix-core
-//   path takes 34 us at N = 16..32; a packed bf16 model instead carries fp32
-//   fragments (bf16 widened exactly) and takes the fragment kernel;
-// * 64 < N <= 256 in fp32, 64 < N <= 128 on a packed bf16 model: the
+//   path takes 34 us at N = 16..32; a packed bf16 model carries bf16
+//   fragments and takes the fragment kernel (9-11 us for N = 16..64);
+// * int8 runs on the fragment kernel only with a packed model (8-10 us for
+//   N <= 64), else on the matrix-core path;
+// * 64 < N <= 256 in fp32, 64 < N <= 128 on a packed bf16 or int8 model: the
 //   matrix-core path has only a few sample tiles (fp32: 138 us for
-//   N = 65..256; bf16: 39 us at N = 65, 46 us at N = 128), while the small path
-//   takes about 20 us per 64 samples, so it runs in 64-sample chunks, one
-//   after another on the stream, when its 64-sample plan runs on the matrix
-//   cores (not the VALU fallback).
+//   N = 65..256; bf16: 39 us at N = 65, 46 us at N = 128; int8: 33-39 us),
+//   while the small path takes 18 us (fp32) or about 10 us (bf16, int8) per
+//   64 samples, so it runs in 64-sample chunks, one after another on the
+//   stream, when its 64-sample plan runs on the matrix cores (not the VALU
+//   fallback).
 enum class Route { kSmall, kSmallChunked, kLarge, kNone };
 constexpr int64_t kSmallMaxNBf16 = 8;
 constexpr int64_t kChunkedMaxN = 256;
 constexpr int64_t kChunkedMaxNBf16 = 128;  // a packed bf16 model's fragment kernel
+constexpr int64_t kChunkedMaxNI8 = 128;    // a packed int8 model's fragment kernel
 
 Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   if (dt == HD_I8) {
@@ -54,6 +58,9 @@ Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
     // (the large-batch bounds on F and D keep every sum exact)
     if (!hd::large_supported(N, F, D, K, dt)) return Route::kNone;
     if (tiled && N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt)) return Route::kSmall;
+    if (tiled && N > hd::kSmallMaxN && N <= kChunkedMaxNI8 &&
+        hd::small_supported(hd::kSmallMaxN, F, D, K, dt))
+      return Route::kSmallChunked;
     return Route::kLarge;
   }
   const bool small_ok = N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt);
@@ -169,9 +176,9 @@ size_t hd_model_packed_bytes(int64_t F, int64_t D, int64_t K, hd_dtype dt) {
 static size_t workspace_need(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool packed,
                              bool det) {
   const Route r = route(N, F, D, K, dt, packed);
-  if (r == Route::kSmall && dt == HD_I8) {
+  if ((r == Route::kSmall || r == Route::kSmallChunked) && dt == HD_I8) {
     // an unaligned X takes the large-batch kernels instead
-    const size_t s = hd::small_workspace_bytes(N, F, D, K, dt, det);
+    const size_t s = hd::small_workspace_bytes(small_n(r, N), F, D, K, dt, det);
     const size_t l = hd::large_workspace_bytes(N, F, D, K, dt);
     return s > l ? s : l;
   }
@@ -230,7 +237,8 @@ static hd_status infer_common(const void* X, const void* B, const void* C, const
     return HD_ERR_ARG;
   Route r = route(N, F, D, K, dt, packed != nullptr);
   if (r == Route::kNone) return HD_ERR_UNSUPPORTED;
-  if (r == Route::kSmall && dt == HD_I8 && (uintptr_t)X % 16 != 0) r = Route::kLarge;
+  if ((r == Route::kSmall || r == Route::kSmallChunked) && dt == HD_I8 && (uintptr_t)X % 16 != 0)
+    r = Route::kLarge;
   const size_t need = workspace_need(N, F, D, K, dt, packed != nullptr, det);
   if (need > 0 && !workspace) return HD_ERR_ARG;
   if (workspace_bytes < need) return HD_ERR_WORKSPACE;

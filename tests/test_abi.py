@@ -198,7 +198,10 @@ def test_int8_limits(L):
     assert _infer(L, dt=I8, K=129) == hd.HD_ERR_UNSUPPORTED
     for n in (1, 9, 32, 64):
         assert L.hd_infer_kernel(n, 561, 10240, 6, I8, 1) == b"small_frag_mfma_kernel"
-    assert L.hd_infer_kernel(65, 561, 10240, 6, I8, 1) == b"large_fused_kernel"
+    # 64 < N <= 128: 64-sample calls of the fragment kernel; above, the large kernels
+    assert L.hd_infer_kernel(65, 561, 10240, 6, I8, 1) == b"small_frag_mfma_kernel"
+    assert L.hd_infer_kernel(128, 561, 10240, 6, I8, 1) == b"small_frag_mfma_kernel"
+    assert L.hd_infer_kernel(129, 561, 10240, 6, I8, 1) == b"large_fused_kernel"
     assert L.hd_infer_kernel(32, 561, 10240, 6, I8, 0) == b"large_fused_kernel"  # raw B, C
     assert L.hd_infer_kernel(32, 1025, 10240, 6, I8, 1) != b"small_frag_mfma_kernel"
     assert L.hd_infer_kernel(32, 561, 10240, 17, I8, 1) == b"large_fused_kernel"

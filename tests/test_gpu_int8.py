@@ -88,6 +88,8 @@ SMALL_CASES = [
     (24, 4, 64, 2),
     (40, 1000, 13000, 5),
     (63, 250, 777, 7),
+    (65, 561, 10240, 6),  # 64 + 1 samples: two calls
+    (128, 617, 4096, 16),  # two 64-sample calls
 ]
 
 

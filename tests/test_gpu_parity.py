@@ -219,6 +219,10 @@ INTEGER = [
     (64, 200, 1000, 12, "f32", True, "small_frag_mfma_kernel"),
     (64, 561, 4096, 6, "f32", True, "small_frag_mfma_kernel"),  # two passes of 32 samples
     (50, 1000, 10240, 6, "f32", True, "small_frag_mfma_kernel"),  # two passes, ragged second
+    # fewer blocks than workgroups on some XCDs (workgroups that own no block),
+    # with two sample passes
+    (64, 700, 1500, 6, "f32", True, "small_frag_mfma_kernel"),
+    (33, 1000, 1500, 5, "f32", True, "small_frag_mfma_kernel"),
     (64, 561, 20480, 6, "f32", True, "small_mfma_kernel"),
     (64, 100, 2048, 17, "f32", False, "small_mfma_kernel"),
     (65, 100, 2048, 17, "f32", False, None),
