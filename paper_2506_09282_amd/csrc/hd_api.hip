@@ -37,18 +37,15 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 //   fragments and takes the fragment kernel (9-11 us for N = 16..64);
 // * int8 runs on the fragment kernel only with a packed model (8-10 us for
 //   N <= 64), else on the matrix-core path;
-// * 64 < N <= 256 in fp32, 64 < N <= 128 on a packed bf16 or int8 model: the
+// * 64 < N <= 256 in fp32 and on a packed bf16 or int8 model: the
 //   matrix-core path has only a few sample tiles (fp32: 138 us for
-//   N = 65..256; bf16: 39 us at N = 65, 46 us at N = 128; int8: 33-39 us),
-//   while the small path takes 18 us (fp32) or about 10 us (bf16, int8) per
-//   64 samples, so it runs in 64-sample chunks, one after another on the
-//   stream, when its 64-sample plan runs on the matrix cores (not the VALU
-//   fallback).
+//   N = 65..256; bf16: 39-47 us; int8: 33-39 us), while the small path takes
+//   18 us (fp32) or about 10 us (bf16, int8) per 64 samples, so it runs in
+//   64-sample chunks, one after another on the stream, when its 64-sample
+//   plan runs on the matrix cores (not the VALU fallback).
 enum class Route { kSmall, kSmallChunked, kLarge, kNone };
 constexpr int64_t kSmallMaxNBf16 = 8;
 constexpr int64_t kChunkedMaxN = 256;
-constexpr int64_t kChunkedMaxNBf16 = 128;  // a packed bf16 model's fragment kernel
-constexpr int64_t kChunkedMaxNI8 = 128;    // a packed int8 model's fragment kernel
 
 Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   if (dt == HD_I8) {
@@ -58,7 +55,7 @@ Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
     // (the large-batch bounds on F and D keep every sum exact)
     if (!hd::large_supported(N, F, D, K, dt)) return Route::kNone;
     if (tiled && N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt)) return Route::kSmall;
-    if (tiled && N > hd::kSmallMaxN && N <= kChunkedMaxNI8 &&
+    if (tiled && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
         hd::small_supported(hd::kSmallMaxN, F, D, K, dt))
       return Route::kSmallChunked;
     return Route::kLarge;
@@ -71,7 +68,7 @@ Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   if (dt == HD_F32 && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
       hd::small_matrix_core(hd::kSmallMaxN, F, D, K, dt, tiled))
     return Route::kSmallChunked;
-  if (dt == HD_BF16 && tiled && N > hd::kSmallMaxN && N <= kChunkedMaxNBf16 &&
+  if (dt == HD_BF16 && tiled && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
       hd::small_matrix_core(hd::kSmallMaxN, F, D, K, dt, tiled))
     return Route::kSmallChunked;
   if (hd::large_supported(N, F, D, K, dt)) return Route::kLarge;

@@ -198,10 +198,10 @@ def test_int8_limits(L):
     assert _infer(L, dt=I8, K=129) == hd.HD_ERR_UNSUPPORTED
     for n in (1, 9, 32, 64):
         assert L.hd_infer_kernel(n, 561, 10240, 6, I8, 1) == b"small_frag_mfma_kernel"
-    # 64 < N <= 128: 64-sample calls of the fragment kernel; above, the large kernels
+    # 64 < N <= 256: 64-sample calls of the fragment kernel; above, the large kernels
     assert L.hd_infer_kernel(65, 561, 10240, 6, I8, 1) == b"small_frag_mfma_kernel"
-    assert L.hd_infer_kernel(128, 561, 10240, 6, I8, 1) == b"small_frag_mfma_kernel"
-    assert L.hd_infer_kernel(129, 561, 10240, 6, I8, 1) == b"large_fused_kernel"
+    assert L.hd_infer_kernel(256, 561, 10240, 6, I8, 1) == b"small_frag_mfma_kernel"
+    assert L.hd_infer_kernel(257, 561, 10240, 6, I8, 1) == b"large_fused_kernel"
     assert L.hd_infer_kernel(32, 561, 10240, 6, I8, 0) == b"large_fused_kernel"  # raw B, C
     assert L.hd_infer_kernel(32, 1025, 10240, 6, I8, 1) != b"small_frag_mfma_kernel"
     assert L.hd_infer_kernel(32, 561, 10240, 17, I8, 1) == b"large_fused_kernel"
@@ -244,13 +244,13 @@ def test_routes_of_new_paths(L):
     """Kernel choice of the bf16 fragment route, the training kernels and the
     int8 variant (host planning only)."""
     k = L.hd_infer_kernel
-    # packed bf16 small batches: the fragment kernel (fp32 fragments); raw: large-batch
+    # packed bf16 small batches: the fragment kernel (bf16 fragments); raw: large-batch
     assert k(32, 561, 10240, 6, hd.HD_BF16, 1) == b"small_frag_mfma_kernel"
     assert k(32, 561, 10240, 6, hd.HD_BF16, 0) == b"large_fused_kernel"
     assert k(32, 561, 10240, 17, hd.HD_BF16, 1) == b"large_fused_kernel"  # K > 16
-    # 64-sample calls of the fragment kernel up to 128 samples of a packed bf16 model
-    assert k(128, 561, 10240, 6, hd.HD_BF16, 1) == b"small_frag_mfma_kernel"
-    assert k(129, 561, 10240, 6, hd.HD_BF16, 1) == b"large_fused_kernel"
+    # 64-sample calls of the fragment kernel up to 256 samples of a packed bf16 model
+    assert k(256, 561, 10240, 6, hd.HD_BF16, 1) == b"small_frag_mfma_kernel"
+    assert k(257, 561, 10240, 6, hd.HD_BF16, 1) == b"large_fused_kernel"
     assert k(100, 561, 10240, 6, hd.HD_BF16, 0) == b"large_fused_kernel"
     b = L.hd_bundle_kernel
     assert b(16384, 3072, 10240, 10, hd.HD_BF16, 1) == b"bundle_dma_kernel"

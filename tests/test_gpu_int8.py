@@ -90,6 +90,7 @@ SMALL_CASES = [
     (63, 250, 777, 7),
     (65, 561, 10240, 6),  # 64 + 1 samples: two calls
     (128, 617, 4096, 16),  # two 64-sample calls
+    (256, 300, 2000, 6),  # four 64-sample calls
 ]
 
 

@@ -236,6 +236,7 @@ INTEGER = [
     (60, 1000, 1500, 5, "bf16", True, "small_frag_mfma_kernel"),  # two sample passes
     (32, 561, 2048, 17, "bf16", True, "large_fused_kernel"),
     (128, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),  # two 64-sample calls
+    (250, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),  # four calls, the last ragged
     (4, 561, 2048, 6, "bf16", True, "small_flat_kernel"),
     (200, 3072, 1024, 10, "bf16", True, "large_chunked_dma_kernel"),
     (130, 2600, 512, 100, "bf16", False, "large_chunked_dma_kernel"),
@@ -264,7 +265,8 @@ TIES = [
     (5, 40, 512, "f32", False, "small_flat_kernel"),
     (200, 40, 512, "f32", False, "small_mfma_kernel"),
     (300, 40, 512, "f32", False, "large_fused_kernel"),
-    (250, 700, 512, "bf16", True, "large_fused_kernel"),
+    (300, 700, 512, "bf16", True, "large_fused_kernel"),
+    (250, 700, 512, "bf16", True, "small_frag_mfma_kernel"),  # four 64-sample calls
     (5, 40, 512, "bf16", False, "small_flat_kernel"),
     (200, 40, 512, "bf16", False, "large_fused_kernel"),
     (32, 40, 512, "f32", True, "small_frag_mfma_kernel"),
