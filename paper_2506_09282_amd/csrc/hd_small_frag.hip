@@ -46,8 +46,8 @@ namespace {
 //     the block's C on the fp32 matrix instruction (Eq. 8).
 // One barrier per block hands red from one role to the other.
 // LDS: red[2][4 waves][NTI][4 q][64 lanes] | cs[cslots][K*16] |
-//      xs: fp32 [NB*F + 16*MS] (+ 4 spare), bf16 [NB*F + 32*MS] (+ 8 spare);
-//      cslots >= blocks per workgroup
+//      xs: fp32 [NB*F + 16*MS] (+ 4 spare), bf16 [NB*F + 32*MS] (+ 8 spare),
+//      int8 [NB*F + 32*MS] (+ 16 spare); cslots >= blocks per workgroup
 // ---------------------------------------------------------------------------
 
 // One block's A operands per lane: MS/4 float4 (fp32), or ceil(MS/8) words
