@@ -251,7 +251,7 @@ static SmallPlan plan_stream(int64_t N, int64_t F, int64_t D, int64_t K, int dt)
   if ((int64_t)p.nblocks * K * kW * 4 >= ((int64_t)1 << 31)) return p;
   const int nti = N <= 16 ? 1 : 2;
   const int64_t nbk = 16 * nti;
-  const int64_t floats = (nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 +
+  const int64_t floats = (2 * nbk * K + 3) / 4 * 4 + 2 * kWaves * nti * 256 +
                          frag_cs_floats((int)cslots, (int)K) +
                          frag_xs_floats((int)nbk, (int)F, ms);
   // the reducer workgroup's eight per-wave sums use the same allocation

@@ -10,7 +10,7 @@
 // into registers once, and then, batch after batch:
 //   - its compute waves run Stage I (Eq. 7) on the matrix cores,
 //   - its finish waves apply HardSign (Eq. 1) and form the block's partial
-//     scores (Eq. 8),
+//     scores (Eq. 8) on the fp32 matrix instruction,
 //   - one wave prefetches the next batch's X into LDS (the queue, Sec. III-A),
 //   - one wave publishes the previous batch's partial scores (fp32 atomics
 //     into one of a few replicas) and then counts itself into that batch's
@@ -24,7 +24,7 @@
 //   wave 0       publisher of batch i-1,
 //   waves 0..3   loaders of batch i+1's X (through registers); wave 1 also
 //                waits on the queue,
-//   waves 2, 3   per-block finish (32 samples x 4 lanes),
+//   waves 2, 3   per-block finish (two of the four column phases each),
 //   waves 4..7   matrix instructions, each over a quarter of F.
 // All waves take part in every barrier; the publisher issues its atomics at
 // the start of a batch and waits for them at its end. The reducer (the last
@@ -95,8 +95,8 @@ __global__ __launch_bounds__(kStreamThreads, 1) void stream_frag_kernel(
   constexpr int NB = 16 * NTI;
   constexpr int G4 = MS / 4;
   extern __shared__ __attribute__((aligned(16))) float smem[];
-  float* sl = smem;                              // [NB*K] scores of the last batch
-  float* red = sl + (NB * K + 3) / 4 * 4;        // [2][4][NTI][16][16]
+  float* sl = smem;                              // [2][NB*K] scores of the last batch
+  float* red = sl + (2 * NB * K + 3) / 4 * 4;    // [2][4][NTI][4][64]
   float* cs = red + 2 * kWaves * NTI * 256;      // C of block i at slot i
   float* xs = cs + frag_cs_floats(cslots, K);    // X, 1 KiB chunks, then a zeroed run
   __shared__ int s_stop;
@@ -292,51 +292,41 @@ __global__ __launch_bounds__(kStreamThreads, 1) void stream_frag_kernel(
       for (int t = 0; t < NTI; ++t)
         acc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.a[g].w, xr[g][t].w, acc[t][1], 0, 0, 0);
     }
-    float4* r = reinterpret_cast<float4*>(red + ((i & 1) * kWaves + cw) * NTI * 256) +
-                (lane & 15) * 4 + (lane >> 4);
+    // lane l holds V^T[d = 4(l/16) + q][n = l%16], q = 0..3; value q goes
+    // to plane q of red[i % 2][cw][t], at position l (conflict-free)
+    float* r = red + ((i & 1) * kWaves + cw) * NTI * 256 + lane;
 #pragma unroll
     for (int t = 0; t < NTI; ++t)
-      r[t * 64] = make_float4(acc[t][0][0] + acc[t][1][0], acc[t][0][1] + acc[t][1][1],
-                              acc[t][0][2] + acc[t][1][2], acc[t][0][3] + acc[t][1][3]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r[t * 256 + q * 64] = acc[t][0][q] + acc[t][1][q];
   };
-  // finish waves 2, 3: thread (n, g), a quad of lanes per sample (as in the
-  // single-batch fragment kernel)
-  const int ft = tid - 128, fn = ft >> 2, fg = ft & 3;
+  // Finish waves 2, 3 (fw = 0, 1): Stage II on the fp32 matrix instruction
+  // (as in the single-batch fragment kernel). Wave fw takes the column
+  // phases q = 2 fw, 2 fw + 1 of every sample tile: lane l sums the four
+  // wave partials of V^T[4(l/16) + q][l%16] (plane q of red), applies
+  // HardSign and feeds it as the B operand of S^T += C_blk · H^T, whose A
+  // operand is C[k = l%16][4(l/16) + q] (rows past K repeat class K-1 and are
+  // never stored). sacc[t] holds S^T[4(l/16) + r][16 t + l%16] over the
+  // workgroup's blocks; the two waves' sums go to their own halves of sl and
+  // are added when they are published.
   const bool finisher = wave == 2 || wave == 3;
-  float sacc[kFragMaxK / 4];
+  const int fw = wave - 2;
+  const float* cl = cs + min(lane & 15, K - 1) * kW + 4 * (lane >> 4);
+  f32x4 sacc[NTI];
 #pragma unroll
-  for (int j = 0; j < kFragMaxK / 4; ++j) sacc[j] = 0.0f;
+  for (int t = 0; t < NTI; ++t) sacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto finish = [&](int i) {
-    if (!finisher || fn >= nb) return;
-    const float4* r4 = reinterpret_cast<const float4*>(red + (i & 1) * kWaves * NTI * 256);
-    const float4* c4 = reinterpret_cast<const float4*>(cs + i * K * kW);
-    float4 v = r4[fn * 4 + fg];
+    if (!finisher) return;  // uniform per wave
+    const float* r = red + (i & 1) * kWaves * NTI * 256 + lane;
 #pragma unroll
-    for (int w = 1; w < kWaves; ++w) {
-      const float4 u = r4[w * NTI * 64 + fn * 4 + fg];
-      v.x += u.x;
-      v.y += u.y;
-      v.z += u.z;
-      v.w += u.w;
-    }
-    const float h0 = activate(v.x, act), h1 = activate(v.y, act), h2 = activate(v.z, act),
-                h3 = activate(v.w, act);
-    // C of eight classes at a time (their reads in flight together), up to
-    // K; classes past K read class 0 and are never stored
+    for (int h = 0; h < 2; ++h) {
+      const int q = 2 * fw + h;
+      const float cv = cl[i * K * kW + q];
 #pragma unroll
-    for (int k0 = 0; k0 < kFragMaxK; k0 += 8) {
-      if (k0 >= K) break;  // uniform
-      float4 c[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) c[j] = c4[(k0 + j < K ? k0 + j : 0) * 4 + fg];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        float d = fmaf(h0, c[j].x, fmaf(h1, c[j].y, fmaf(h2, c[j].z, h3 * c[j].w)));
-        d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                           0, __builtin_bit_cast(int, d), 0xB1, 0xf, 0xf, false));
-        d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                           0, __builtin_bit_cast(int, d), 0x4E, 0xf, 0xf, false));
-        sacc[(k0 + j) >> 2] += ((k0 + j) & 3) == fg ? d : 0.0f;
+      for (int t = 0; t < NTI; ++t) {
+        const float* p = r + t * 256 + q * 64;
+        const float v = (p[0] + p[NTI * 256]) + (p[2 * NTI * 256] + p[3 * NTI * 256]);
+        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(cv, activate(v, act), sacc[t], 0, 0, 0);
       }
     }
   };
@@ -347,7 +337,7 @@ __global__ __launch_bounds__(kStreamThreads, 1) void stream_frag_kernel(
   auto publish_issue = [&](int b) {
     float* rep = reinterpret_cast<float*>(wsb + kLine + (size_t)b * bbytes + kLine);
     float* my = rep + (int64_t)(blockIdx.x % R) * NK;
-    for (int p = lane; p < npairs; p += kWave) publish_add(my + p, sl[p]);
+    for (int p = lane; p < npairs; p += kWave) publish_add(my + p, sl[p] + sl[NB * K + p]);
   };
   auto publish_done = [&](int b) {
     unsigned* counter = reinterpret_cast<unsigned*>(wsb + kLine + (size_t)b * bbytes);
@@ -404,13 +394,19 @@ __global__ __launch_bounds__(kStreamThreads, 1) void stream_frag_kernel(
       raw_barrier();
     }
     if (nmine > 0) finish(nmine - 1);  // a workgroup may own no block (it publishes zeros)
-    if (finisher && fn < nb) {
+    if (finisher) {
+      float* slw = sl + fw * (NB * K);
 #pragma unroll
-      for (int k = 0; k < kFragMaxK; ++k)
-        if (k < K && (k & 3) == fg) sl[fn * K + k] = sacc[k >> 2];
+      for (int t = 0; t < NTI; ++t) {
+        const int n = 16 * t + (lane & 15);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int k = 4 * (lane >> 4) + r;
+          if (k < K && n < nb) slw[n * K + k] = sacc[t][r];
+        }
+        sacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
     }
-#pragma unroll
-    for (int j = 0; j < kFragMaxK / 4; ++j) sacc[j] = 0.0f;
     if (wave == 0 && b > 0) publish_done(b - 1);
     if (next0 == 1) x_store(tid);  // X of batch b+1 (the compute waves hold b's)
     if (wave == 1 && next0 == 0) {
