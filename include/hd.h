@@ -64,16 +64,19 @@ typedef enum {
  * HD_I8: the int8 model variant (the quantised models of Sec. II-C, which the
  * paper mentions and does not use): X, B and C hold int8 values; Stage I sums
  * exactly in int32 on the int8 matrix instructions, HardSign is taken on the
- * exact sum, and Stage II is exact in fp32 (C widened to bf16, exact for
- * int8). Every result is therefore exact: scores are integers, and labels and
+ * exact sum, and Stage II is exact in fp32 (C widened exactly to bf16 or
+ * fp32). Every result is therefore exact: scores are integers, and labels and
  * scores equal the mathematical definition bit for bit. Scales of a
  * quantised model do not enter: a positive scale of X or B leaves every
  * HardSign unchanged, and a per-class scale of C is the caller's to apply to
  * the returned scores. Supported by hd_pack_model, hd_infer, hd_infer_packed,
  * hd_infer_packed_noalloc, hd_bundle_classes_packed and the size and kernel
  * queries, with HD_ACT_HARDSIGN, K <= 128, F <= 131071 (|sum| < 2^31) and
- * D <= 131072 (|score| <= 2^24); every batch size runs on the large-batch
- * kernels. Elsewhere HD_ERR_UNSUPPORTED.
+ * D <= 131072 (|score| <= 2^24). Small batches on a packed model (N <= 256,
+ * K <= 16, F <= 1024, X 16-byte aligned) run on the small-batch fragment
+ * kernel (int8 matrix instructions, exact int32 sums converted exactly to
+ * fp32), everything else on the large-batch kernels; the workspace queries
+ * cover both. Elsewhere HD_ERR_UNSUPPORTED.
  */
 typedef enum { HD_F32 = 0, HD_BF16 = 1, HD_I8 = 2 } hd_dtype;
 
