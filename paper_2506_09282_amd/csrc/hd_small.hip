@@ -85,11 +85,13 @@ size_t frag_bytes(int64_t F, int64_t D, int dt) {
   return (size_t)cdiv(D, kW) * 256 * ms * sizeof(float);
 }
 
-// Kernel choice: N <= 8 takes the flat kernel; fp32 with 8 < N <= 64 a
-// matrix-core kernel (the fragment kernel on a packed model, else the block
-// kernel for N <= 32 or the persistent one) when its LDS fits; raw matrices
-// with unaligned bases or D % 4 != 0 (kRawScalar) and everything else take
-// the VALU kernel.
+// Kernel choice: on a packed model the fragment kernel for N > 4 (every N
+// for int8) when its LDS fits (at N = 8: fp32 10.8 us, bf16 9.0 us, against
+// 11.6 and 10.8 us on the flat kernel); otherwise N <= 8 takes the flat
+// kernel; fp32 with 8 < N <= 64 a matrix-core kernel (the block kernel for
+// N <= 32 or the persistent one) when its LDS fits; raw matrices with
+// unaligned bases or D % 4 != 0 (kRawScalar) and everything else take the
+// VALU kernel.
 SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay, bool x_aligned) {
   if (lay == kRawScalar) return plan_valu(N, F, D, K, 2);
   SmallPlan v = plan_valu(N, F, D, K, 8);
@@ -97,7 +99,7 @@ SmallPlan plan_small(int64_t N, int64_t F, int64_t D, int64_t K, int dt, int lay
   SmallPlan p{};
   p.nblocks = v.nblocks;
   // int8 runs only on the fragment kernel, for every N
-  if (lay == kTiled && x_aligned && (N > 8 || dt == 2) && frag_ms(F) > 0) {
+  if (lay == kTiled && x_aligned && (N > 4 || dt == 2) && frag_ms(F) > 0) {
     const int ms = frag_ms(F);
     int64_t cslots = 1;  // the most blocks any workgroup walks
     for (int b = 0; b < v.grid; ++b) {

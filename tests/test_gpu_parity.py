@@ -238,6 +238,9 @@ INTEGER = [
     (128, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),  # two 64-sample calls
     (250, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),  # four calls, the last ragged
     (4, 561, 2048, 6, "bf16", True, "small_flat_kernel"),
+    # 4 < N <= 8 on a packed model: the fragment kernel with one partly used tile
+    (5, 561, 2048, 6, "bf16", True, "small_frag_mfma_kernel"),
+    (8, 561, 10240, 6, "f32", True, "small_frag_mfma_kernel"),
     (200, 3072, 1024, 10, "bf16", True, "large_chunked_dma_kernel"),
     (130, 2600, 512, 100, "bf16", False, "large_chunked_dma_kernel"),
     (200, 3072, 1024, 10, "f32", True, "large_chunked_kernel"),
