@@ -45,10 +45,11 @@ def test_status_strings(L):
 def test_workspace_sizes(L):
     # small batch: 256-byte ticket header + replicated accumulators
     small = L.hd_infer_workspace_bytes(32, 561, 10240, 6, hd.HD_F32)
-    # counters, then the score replicas: 32 (default mode) or one per
-    # workgroup (at most one per 16-column block) plus one per ticket group
-    # (deterministic mode); the query covers both
-    assert small == 256 * 33 + 4 * max(32, 10240 // 16 + 32) * 32 * 6
+    # counters (the final one and 8 group counters, 256 bytes each), then the
+    # score replicas: 32 (default mode) or one per workgroup (at most one per
+    # 16-column block) plus one per ticket group (deterministic mode); the
+    # query covers both
+    assert small == 256 * 9 + 4 * max(32, 10240 // 16 + 8) * 32 * 6
     assert L.hd_infer_workspace_bytes(0, 561, 10240, 6, hd.HD_F32) == 0
     assert L.hd_infer_workspace_bytes(5, 0, 10, 6, hd.HD_F32) == 0
     # large batch, raw entry: holds the tiled model
