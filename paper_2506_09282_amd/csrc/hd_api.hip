@@ -51,8 +51,8 @@ Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   if (dt == HD_I8) {
     // int8 on a packed model: the fragment kernel for small batches (it takes
     // 16-byte aligned X; others fall back to the large-batch kernels, which
-    // the workspace query covers as well)
-    // (the large-batch bounds on F and D keep every sum exact)
+    // the workspace query covers as well). The large-batch bounds on F and D
+    // keep every sum exact, on either path.
     if (!hd::large_supported(N, F, D, K, dt)) return Route::kNone;
     if (tiled && N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt)) return Route::kSmall;
     if (tiled && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
@@ -62,7 +62,7 @@ Route route(int64_t N, int64_t F, int64_t D, int64_t K, int dt, bool tiled) {
   }
   const bool small_ok = N <= hd::kSmallMaxN && hd::small_supported(N, F, D, K, dt);
   if (small_ok && (dt == HD_F32 || N <= kSmallMaxNBf16)) return Route::kSmall;
-  // a packed bf16 model carries fp32 fragments: the fragment kernel serves it
+  // a packed bf16 model carries bf16 fragments: the fragment kernel serves it
   if (small_ok && dt == HD_BF16 && tiled && hd::small_matrix_core(N, F, D, K, dt, tiled))
     return Route::kSmall;
   if (dt == HD_F32 && N > hd::kSmallMaxN && N <= kChunkedMaxN &&
